@@ -1,0 +1,27 @@
+"""CPU oracle for the Trivance AllReduce (Juerss, Addanki, Schmid, arXiv 2602.17254).
+
+TEST INFRASTRUCTURE ONLY. This package is a plain, slow, obviously-correct CPU model of what the
+emulated AllReduce computes. Only the test suite, the smoke check and the CPU-baseline leg of the
+benchmark may import it. The product path (the HIP library and its Python binding) never imports,
+calls or falls back to anything in here, and nothing in here imports the product path: the two
+share no code. The seeded input generators live in a module of their own that holds none of the
+method's arithmetic.
+
+Modules
+-------
+schedule    peers, per-step distances, torus dimension rotation, reachability (Algorithm 1) and
+            the closed-form block sets of Sec. 4.3.
+partition   the rule that splits a rank's vector into per-collective segments and blocks
+            (the paper assumes m/n-sized blocks; the rounding rule is a reading, see the module).
+allreduce   message-passing emulation of both variants, step by step, with an explicit
+            barrier between posting and reducing (Sec. 4.1, 4.2, 4.3, 5), plus reference sums.
+congestion  hop-by-hop link-load walk (cost model of Sec. 2.1) and the transmission-delay
+            factors of Tables 1 and 2 / Appendix B.
+
+Parity status: every function here is pinned by a `-m "not gpu"` test against values the paper
+prints, closed forms or brute force, except the floating-point summation order of the joint
+reduction, which the paper leaves open; that order is a stated reading (own + left) + right,
+pinned only through the invariants listed in tests/test_oracle_allreduce.py.
+"""
+
+from . import schedule, partition, allreduce, congestion  # noqa: F401
