@@ -1,0 +1,234 @@
+"""Benchmark of the emulated Trivance AllReduce on one MI355X.
+
+python bench.py [--steps K] [--warmup W] [--workload NAME | --all] [--no-cpu-baseline]
+
+A step is one whole emulated AllReduce (every pass of the schedule) over the workload's n rank
+vectors, which are resident in HBM before timing starts. K steps are timed back to back, bracketed
+by device synchronisation; each pass is bracketed by HIP events on the stream it runs on, which
+gives the per-launch kernel durations used for the roofline. Throughput counts the algorithmic
+bytes of the step-by-step schedule (each participating location read once and each output
+written once per pass; trivance_algorithmic_bytes).
+
+Default workload: 81 virtual ranks on a ring, latency-optimal variant, 8 MiB fp32 per rank.
+Prints one JSON line per workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2602_17254_amd import inputs  # noqa: E402
+
+METRIC = "emulated AllReduce HBM GB/s and % of HBM peak, per-rank 8-128 MiB, 1 GPU"
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
+
+# HBM traffic per launch measured with rocprofv3 --pmc (FETCH_SIZE / WRITE_SIZE, scaled by the
+# same counters read for a plain copy of known size), keyed by kernel, valid only for the kernel
+# source it was measured on (sha256 of the source file, first 16 hex digits).
+MEASURED_TRAFFIC = {}
+
+
+def _src_sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def _say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, gpu_first_result_cols, cols, V_cols, seconds_target=15.0):
+    """Time the CPU oracle (as it stands, single-threaded numpy) on a column sample of the same
+    workload, and compare its result with the GPU's first AllReduce on those columns."""
+    from oracle import allreduce, partition
+
+    D = len(w.dims)
+    seg, blk = partition.column_labels(w.elems, D, w.n, cols)
+    t0 = time.perf_counter()
+    if w.variant == "L":
+        out = allreduce.latency_optimal(V_cols, w.dims, col_seg=seg)
+    else:
+        out = allreduce.bandwidth_optimal(V_cols, w.dims, col_seg=seg, col_blk=blk)
+    dt = time.perf_counter() - t0
+    S = sum(int(round(np.log(d) / np.log(3))) for d in w.dims)
+    # algorithmic bytes of the sample (same formula as the device path)
+    ncols = len(cols)
+    if w.variant == "L":
+        sample_bytes = 2 * S * w.n * ncols * 4
+    else:
+        sample_bytes = int(3.5 * 4 * ncols * (w.n - 1))
+    same = bool(np.array_equal(out, gpu_first_result_cols))
+    return {
+        "value": round(sample_bytes / dt / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{ncols} of {w.elems} columns x {w.n} ranks (all passes), {dt:.2f} s",
+        "seconds": round(dt, 3),
+        "matches_gpu_on_sample": same,
+    }
+
+
+def _sample_for_baseline(w, budget_cols):
+    rng = np.random.default_rng(w.seed + 99)
+    if budget_cols >= w.elems:
+        return np.arange(w.elems, dtype=np.int64)
+    start = int(rng.integers(0, w.elems - budget_cols))
+    return np.arange(start, start + budget_cols, dtype=np.int64)
+
+
+def run_workload(w, steps, warmup, with_cpu):
+    import torch
+
+    import paper_2602_17254_amd as T
+
+    torch.cuda.set_device(0)
+    plan = T.trivance_plan(w.dims, w.variant)
+    P = plan.num_passes
+    alg_bytes = T.trivance_algorithmic_bytes(plan, w.elems)
+    pass_bytes = [T.trivance_pass_bytes(plan, w.elems, p) for p in range(P)]
+
+    # ---- inputs resident in HBM (untimed) ----
+    _say(f"[bench] {w.name}: preparing inputs ({w.n} x {w.elems} fp32)")
+    buf = torch.empty((w.n, w.elems), dtype=torch.float32, device="cuda")
+    if w.dist == "hash_uniform":
+        T.trivance_fill_hash_uniform(buf, w.seed)
+        V_host = None
+    else:
+        V_host = inputs.normal_f32(w.seed, w.n, w.elems)
+        buf.copy_(torch.from_numpy(V_host))
+    torch.cuda.synchronize()
+
+    # ---- first run: result kept for the CPU-baseline comparison ----
+    budget = {"L": 2_097_152, "B": 60_000}[w.variant]
+    cols = _sample_for_baseline(w, min(budget, w.elems))
+    if V_host is not None:
+        V_cols = np.ascontiguousarray(V_host[:, cols])
+    else:
+        V_cols = inputs.hash_uniform(w.seed, w.elems, np.arange(w.n), cols)
+    del V_host
+    T.trivance_allreduce_emulated(buf, plan)
+    torch.cuda.synchronize()
+    first_cols = buf.index_select(1, torch.from_numpy(cols).cuda()).cpu().numpy()
+
+    # ---- warmup ----
+    for _ in range(warmup):
+        T.trivance_allreduce_emulated(buf, plan)
+    torch.cuda.synchronize()
+
+    # ---- timed region: K steps, every pass bracketed by events on the launch stream ----
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(P + 1)] for _ in range(steps)]
+    _say(f"[bench] {w.name}: timing {steps} steps x {P} passes")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        for p in range(P):
+            ev[k][p].record(stream)
+            T.trivance_allreduce_emulated_steps(buf, plan, p, p + 1, stream)
+        ev[k][P].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_pass_ms = np.array([[ev[k][p].elapsed_time(ev[k][p + 1]) for p in range(P)]
+                            for k in range(steps)])
+    ms_per_step = wall * 1e3 / steps
+    value = alg_bytes / (ms_per_step * 1e-3) / 1e9
+
+    # dominant kernel: the pass type with the most total time
+    phases = [T.trivance_plan_step(plan, p)[0] for p in range(P)]
+    names = {0: "latency_step_kernel", 1: "block_step_kernel<reduce>", 2: "block_step_kernel<copy>"}
+    tot = {}
+    for p, ph in enumerate(phases):
+        tot.setdefault(ph, [0.0, 0, 0])
+        tot[ph][0] += per_pass_ms[:, p].sum()
+        tot[ph][1] += steps
+        tot[ph][2] += pass_bytes[p] * steps
+    dom = max(tot, key=lambda ph: tot[ph][0])
+    dom_ms = tot[dom][0] / tot[dom][1]
+    dom_bytes = tot[dom][2] / tot[dom][1]
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    src = os.path.join(ROOT, "paper_2602_17254_amd", "csrc", "executor.hip")
+    meas = MEASURED_TRAFFIC.get((w.name, names[dom]))
+    traffic = None
+    if meas and meas["src_sha"] == _src_sha(src):
+        traffic = meas["bytes_per_launch"]
+    roofline = {
+        "bound": "hbm",
+        "kernel": names[dom],
+        "achieved": round(achieved, 1),
+        "peak": HBM_PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBPS, 4),
+        "traffic": traffic,
+        "alg_bytes_per_launch": int(dom_bytes),
+        "avg_launch_ms": round(dom_ms, 4),
+    }
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "topology": "x".join(map(str, w.dims)),
+            "variant": {"L": "latency-optimal", "B": "bandwidth-optimal"}[w.variant],
+            "n_ranks": w.n,
+            "elems_per_rank": w.elems,
+            "rank_bytes": w.rank_bytes,
+            "passes": P,
+            "alg_bytes_per_step": alg_bytes,
+            "input": w.dist,
+        },
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
+        "per_pass_ms": [round(float(x), 4) for x in per_pass_ms.mean(axis=0)],
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    del buf
+    torch.cuda.empty_cache()
+    if with_cpu:
+        _say(f"[bench] {w.name}: CPU oracle on {len(cols)} columns")
+        line["cpu_baseline"] = cpu_baseline(w, first_cols, cols, V_cols)
+    return line
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=inputs.HEADLINE, choices=sorted(inputs.WORKLOADS))
+    ap.add_argument("--all", action="store_true", help="every named workload, one line each")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures a single-GPU emulation of all virtual ranks; it runs on exactly "
+              "one GPU (--gpus 1).", file=sys.stderr)
+        sys.exit(2)
+    names = list(inputs.WORKLOADS) if args.all else [args.workload]
+    for name in names:
+        line = run_workload(inputs.WORKLOADS[name], args.steps, args.warmup,
+                            with_cpu=not args.no_cpu_baseline)
+        print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

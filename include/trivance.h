@@ -1,0 +1,207 @@
+/*
+ * trivance.h -- C ABI of the MI355X (gfx950) emulated Trivance AllReduce.
+ *
+ * Trivance (Juerss, Addanki, Schmid, arXiv 2602.17254) is an AllReduce for bidirectional rings
+ * and tori: at step k every rank exchanges data with the two peers at distance 3^k in opposite
+ * directions and reduces both incoming messages together with its own partial result (a "joint
+ * reduction"), finishing in log3(n) steps (Sec. 4). This library executes that schedule for n
+ * *virtual* ranks whose vectors all live in one GPU's memory: a "send" is a read of another
+ * rank's row, and every step is materialised in HBM before the next one starts (the per-step
+ * barrier of Sec. 4.3 is a kernel boundary).
+ *
+ * Conventions for every function:
+ *   - return value 0 (TRIVANCE_OK) on success, a negative trivance_status on failure;
+ *   - pointers documented as "device" must point to GPU memory of the current HIP device,
+ *     pointers documented as "host" to ordinary CPU memory;
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream);
+ *   - nothing is retained after return except what a plan owns.
+ * Nothing here depends on PyTorch; the Python binding only marshals arguments.
+ */
+#ifndef TRIVANCE_H
+#define TRIVANCE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TRIVANCE_MAX_DIMS 8
+
+/* Opaque, immutable schedule. May be shared by threads and streams once created. */
+typedef struct trivance_plan trivance_plan_t;
+
+typedef enum {
+    TRIVANCE_LATENCY_OPT = 0,   /* Sec. 4.2: whole segments every step, log3(n) passes        */
+    TRIVANCE_BANDWIDTH_OPT = 1, /* Sec. 4.1: reduce-scatter then all-gather, 2 log3(n) passes */
+    TRIVANCE_BRUCK_REF = 2      /* Sec. 2.4 / Fig. 1 comparison pattern on a ring: offsets
+                                   +3^k and +2*3^k. Congestion counting only; not executable. */
+} trivance_variant;
+
+typedef enum { TRIVANCE_F32 = 0, TRIVANCE_I32 = 1 } trivance_dtype;
+
+typedef enum {
+    TRIVANCE_ROUTE_SCHEDULED = 0, /* a message travels in the direction of its offset's sign   */
+    TRIVANCE_ROUTE_SHORTEST = 1   /* the shorter way round its ring; a tie keeps the sign
+                                     (Appendix C's rerouted Bruck; Appendix E)                 */
+} trivance_routing;
+
+typedef enum {
+    TRIVANCE_PHASE_LATENCY = 0,        /* one step of the latency-optimal variant   */
+    TRIVANCE_PHASE_REDUCE_SCATTER = 1, /* one reduce-scatter step (joint reduction) */
+    TRIVANCE_PHASE_ALLGATHER = 2       /* one all-gather step (copies only)         */
+} trivance_phase;
+
+typedef struct {
+    int ndims;                   /* must equal the plan's number of dimensions */
+    int dims[TRIVANCE_MAX_DIMS]; /* must equal the plan's sides                 */
+    int routing;                 /* a trivance_routing                          */
+} trivance_topology;
+
+typedef enum {
+    TRIVANCE_OK = 0,
+    TRIVANCE_EINVAL = -1,      /* bad argument: NULL pointer, sizes that do not match, ranges  */
+    TRIVANCE_EUNSUPPORTED = -2,/* valid request outside what is implemented (see each call)    */
+    TRIVANCE_EHIP = -3,        /* the HIP runtime reported an error (launch, copy, allocation) */
+    TRIVANCE_ENOMEM = -4,      /* host memory allocation failed                                */
+    TRIVANCE_ESIZE = -5        /* caller-provided output is too small                          */
+} trivance_status;
+
+/*
+ * trivance_plan -- build the step / peer / block schedule (host only, no GPU work).
+ *
+ *   n           number of virtual ranks; must equal the product of the sides.
+ *   torus_dims  host array of ndims sides, dimension 0 varying fastest in the rank numbering
+ *               (rank = x_0 + n_0 * (x_1 + n_1 * (...))). ndims == 0 or torus_dims == NULL
+ *               means a ring of n.
+ *   variant     a trivance_variant.
+ *   out         receives the new plan; release it with trivance_plan_destroy.
+ *
+ * Schedule (Sec. 4.1 peers pi(r,k) = r -/+ 3^k; Theorem 1 step count; Sec. 5 tori): S = log3(n)
+ * steps. On a D-dimensional torus D collectives run concurrently, collective c on segment c of
+ * every vector; at global step t collective c works on dimension (c + t) mod D at distance
+ * 3^(t div D) (Sec. 5 dimension switching, Appendix B step index t = d + D k).
+ *
+ * Errors: EINVAL for out == NULL, n < 1, ndims < 0, a side < 1, product != n;
+ *         EUNSUPPORTED for a side that is not a power of three (Sec. 4.4's final-step rule is not
+ *         implemented), unequal sides (no rotation rule in the paper), ndims > TRIVANCE_MAX_DIMS,
+ *         or TRIVANCE_BRUCK_REF on more than one dimension.
+ */
+int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance_plan_t** out);
+
+/* Release a plan (NULL is ignored). */
+void trivance_plan_destroy(trivance_plan_t* plan);
+
+/* Number of steps S = log3(n) (>= 0), or a negative status for plan == NULL. */
+int trivance_plan_num_steps(const trivance_plan_t* plan);
+
+/* Number of passes (kernel-materialised steps): S for latency-optimal and Bruck, 2 S for
+ * bandwidth-optimal (S reduce-scatter steps, then S all-gather steps in reverse order). */
+int trivance_plan_num_passes(const trivance_plan_t* plan);
+
+/*
+ * trivance_plan_step -- introspection of one pass for one collective.
+ *   phase    <- a trivance_phase
+ *   step     <- global step index t (all-gather passes run t = S-1 .. 0)
+ *   dim      <- torus dimension used by this collective in this pass
+ *   distance <- peer distance 3^(t div D)
+ * Any output pointer may be NULL. EINVAL if pass or collective is out of range.
+ */
+int trivance_plan_step(const trivance_plan_t* plan, int pass, int collective, int* phase,
+                       int* step, int* dim, int* distance);
+
+/*
+ * trivance_block_range -- element range [begin, end) of block `block` in segment `collective`
+ * for vectors of `elems` elements. The paper assumes blocks of m/n (Sec. 2.2, 4.1); the rounding
+ * rule used here: 64-element granules, G = ceil(elems / 64); segment c holds granules
+ * [floor(c G / D), floor((c+1) G / D)); block j of a G_c-granule segment holds its granules
+ * [floor(j G_c / n), floor((j+1) G_c / n)); bounds are clipped at elems. Blocks may be empty.
+ * block == -1 returns the whole segment. Block j is owned (finished) by rank j.
+ * EINVAL for a NULL output, elems < 0, or an index out of range.
+ */
+int trivance_block_range(const trivance_plan_t* plan, int64_t elems, int collective, int block,
+                         int64_t* begin, int64_t* end);
+
+/*
+ * trivance_algorithmic_bytes -- bytes the step-by-step schedule must move through memory for one
+ * AllReduce of `elems` elements per rank (each participating location read once and each output
+ * written once per pass). Latency-optimal: 2 S n elems w. Bandwidth-optimal: reduce-scatter step t
+ * reads n elems w / 3^t and writes a third of that; all-gather step t reads n elems w / 3^(t+1)
+ * and writes twice that; in total 3.5 w elems (n - 1) for divisible sizes (the exact sum over the
+ * actual blocks is returned). w = 4 for both dtypes. Negative status on bad arguments.
+ */
+int64_t trivance_algorithmic_bytes(const trivance_plan_t* plan, int64_t elems, int dtype);
+
+/* Same accounting for a single pass (0 <= pass < num_passes). */
+int64_t trivance_pass_bytes(const trivance_plan_t* plan, int64_t elems, int dtype, int pass);
+
+/*
+ * trivance_allreduce_emulated -- run the whole schedule, in place, on n virtual ranks.
+ *
+ *   buffers  device array of n * elems values, rank-major: rank r's vector is
+ *            buffers[r * elems .. (r + 1) * elems). Caller-owned; updated in place.
+ *   n        number of ranks (must match the plan).
+ *   elems    elements per rank (>= 0).
+ *   dtype    TRIVANCE_F32 or TRIVANCE_I32 (int32 adds wrap modulo 2^32).
+ *   plan     a latency- or bandwidth-optimal plan.
+ *   stream   hipStream_t (NULL = default stream).
+ *
+ * Semantics (Sec. 2.2, 4.1-4.3, 5): integer results equal the exact column sums on every rank.
+ * Float results follow the schedule: each joint reduction computes (own + left) + right with
+ * left the peer at -distance, in IEEE fp32 round-to-nearest-even, no fused or reordered adds.
+ * The latency-optimal variant leaves ranks with (legitimately) different float bits; the
+ * bandwidth-optimal one leaves identical bits on every rank.
+ *
+ * Asynchronous: all passes are enqueued on `stream` and the call returns; execution errors
+ * surface on stream synchronisation. No device memory is allocated and no host synchronisation
+ * happens. n == 1 or elems == 0 is a valid no-op. Calls that overlap on the same buffers race.
+ * Errors: EINVAL (NULL plan/buffers with elems > 0, n mismatch, elems < 0, bad dtype),
+ * EUNSUPPORTED (a Bruck plan, sizes beyond 32-bit work-unit counts), EHIP (launch failure).
+ */
+int trivance_allreduce_emulated(void* buffers, int n, int64_t elems, int dtype,
+                                const trivance_plan_t* plan, void* stream);
+
+/* Same, running only passes [pass_begin, pass_end) (0 <= begin <= end <= num_passes); used to
+ * inspect or resume the state between steps. Running all ranges back to back equals one full
+ * call. */
+int trivance_allreduce_emulated_steps(void* buffers, int n, int64_t elems, int dtype,
+                                      const trivance_plan_t* plan, void* stream, int pass_begin,
+                                      int pass_end);
+
+/*
+ * trivance_congestion -- per-pass, per-directed-link message counts (Sec. 2.1: c_k = number of
+ * chunks sharing a link), computed on the GPU and copied to a host array. Synchronous.
+ *
+ *   topo       sides (must equal the plan's) and routing; NULL = the plan's sides, scheduled
+ *              routing.
+ *   loads      host int64 array [passes][n][2 D]; entry [p][r][2d] counts messages crossing the
+ *              link that leaves rank r towards +d in pass p, [p][r][2d+1] towards -d.
+ *   loads_len  number of entries available.
+ *
+ * loads == NULL returns the required length (positive). ESIZE if loads_len is too small,
+ * EUNSUPPORTED for a side above 6561. Allocates and frees a temporary device buffer.
+ */
+int64_t trivance_congestion(const trivance_plan_t* plan, const trivance_topology* topo,
+                            int64_t* loads, int64_t loads_len);
+
+/* Asynchronous form writing the same array into caller-owned device memory `loads_dev` on
+ * `stream`; allocates nothing. */
+int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topology* topo,
+                               int64_t* loads_dev, int64_t loads_len, void* stream);
+
+/*
+ * trivance_fill_hash_uniform -- input generator (not part of the AllReduce): writes U(-1, 1)
+ * fp32 values to the device array `buffers` of n * elems floats, value (r, e) being the k-th
+ * output of SplitMix64 (Steele, Lea, Flood 2014) started from state 0 with
+ * k = seed * 2^40 + r * elems + e + 1, mapped to (h >> 40) * 2^-23 - 1. Asynchronous on stream.
+ */
+int trivance_fill_hash_uniform(void* buffers, int n, int64_t elems, uint64_t seed, void* stream);
+
+/* Static description of a status code. */
+const char* trivance_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TRIVANCE_H */

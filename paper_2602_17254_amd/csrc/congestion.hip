@@ -1,0 +1,211 @@
+// Per-link congestion counter of a Trivance (or Bruck comparison) schedule, on the GPU.
+//
+// Sec. 2.1: the congestion of a step is the number of chunks (messages) sharing a link. The
+// network is a ring or torus with one port per direction and dimension; every transmission stays
+// inside one dimension (Appendix E). In each pass every rank sends, for every collective, one
+// message per offset along that collective's active dimension: offsets -3^k and +3^k for
+// Trivance (Sec. 4.1), +3^k and +2*3^k for the Bruck comparison pattern (Sec. 2.4, Fig. 1).
+//
+// One 64-thread workgroup handles one (pass, dimension, line) triple, a line being the ring of
+// ranks that differ only in that dimension's coordinate. Each message adds +1 over a cyclic range
+// of directed links; the workgroup records the range ends in an LDS difference array (plus a
+// count of ranges that wrap past position 0) and turns it into per-link loads with a wavefront
+// inclusive scan. Every output entry is written, so no clearing pass is needed.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "plan.h"
+
+namespace trivance {
+namespace {
+
+constexpr int kMaxPasses = 48;
+constexpr int kMaxSide = 6561;  // LDS: two difference arrays of side + 1 ints
+
+struct CongArgs {
+    int n;
+    int D;
+    int npasses;
+    int bruck;
+    int shortest;
+    int lines;  // lines per dimension: n / side
+    int dims[kMaxDims];
+    int strides[kMaxDims];
+    int distance[kMaxPasses];
+    int act_dim[kMaxPasses][kMaxDims];
+};
+
+// Direction (+1 / -1) and hop count of a message over `offset` on a ring of `side` nodes.
+__device__ __forceinline__ void route(int offset, int side, bool shortest, int* dir, int* hops) {
+    int fwd = offset % side;
+    if (fwd < 0) fwd += side;
+    if (fwd == 0) {
+        *dir = 1;
+        *hops = 0;
+        return;
+    }
+    const int back = side - fwd;
+    if (!shortest) {
+        *dir = offset > 0 ? 1 : -1;
+        *hops = offset > 0 ? offset : -offset;
+        return;
+    }
+    if (fwd < back) {
+        *dir = 1;
+        *hops = fwd;
+    } else if (back < fwd) {
+        *dir = -1;
+        *hops = back;
+    } else {
+        *dir = offset > 0 ? 1 : -1;
+        *hops = fwd;
+    }
+}
+
+// +1 on the cyclic link range [s, s + len) of a line with `side` positions.
+__device__ __forceinline__ void add_range(int* diff, int* wraps, int s, int len, int side) {
+    const int e = s + len;
+    atomicAdd(&diff[s], 1);
+    if (e <= side) {
+        atomicAdd(&diff[e], -1);  // diff[side] is a sentinel, never read back
+    } else {
+        atomicAdd(wraps, 1);
+        atomicAdd(&diff[e - side], -1);
+    }
+}
+
+__global__ __launch_bounds__(64) void congestion_kernel(int64_t* __restrict__ loads, CongArgs a) {
+    extern __shared__ int lds[];
+    const int lane = threadIdx.x;
+    const uint32_t wg = blockIdx.x;
+    const int line = (int)(wg % (uint32_t)a.lines);
+    const uint32_t rest = wg / (uint32_t)a.lines;
+    const int dim = (int)(rest % (uint32_t)a.D);
+    const int pass = (int)(rest / (uint32_t)a.D);
+
+    const int side = a.dims[dim];
+    const int stride = a.strides[dim];
+    const int line_base = (line % stride) + (line / stride) * stride * side;
+    int* plus = lds;               // side + 1 entries
+    int* minus = lds + side + 1;   // side + 1 entries
+    int* wraps = lds + 2 * side + 2;  // [0] plus, [1] minus
+
+    for (int x = lane; x < 2 * side + 4; x += 64) lds[x] = 0;
+    __syncthreads();
+
+    const int dist = a.distance[pass];
+    for (int x = lane; x < side; x += 64) {
+        for (int c = 0; c < a.D; ++c) {
+            if (a.act_dim[pass][c] != dim) continue;
+            const int off0 = a.bruck ? dist : -dist;
+            const int off1 = a.bruck ? 2 * dist : dist;
+            for (int m = 0; m < 2; ++m) {
+                int dir, hops;
+                route(m == 0 ? off0 : off1, side, a.shortest != 0, &dir, &hops);
+                if (hops == 0) continue;
+                if (dir > 0) {
+                    add_range(plus, &wraps[0], x, hops, side);
+                } else {
+                    // links leaving x, x-1, ..., x-hops+1 towards -dim
+                    int s = x - hops + 1;
+                    if (s < 0) s += side;
+                    add_range(minus, &wraps[1], s, hops, side);
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    const int port_plus = 2 * dim;
+    const int64_t row = (int64_t)pass * a.n;
+    for (int sgn = 0; sgn < 2; ++sgn) {
+        const int* diff = sgn == 0 ? plus : minus;
+        int carry = wraps[sgn];
+        for (int x0 = 0; x0 < side; x0 += 64) {
+            const int x = x0 + lane;
+            int v = x < side ? diff[x] : 0;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int t = __shfl_up(v, off, 64);
+                if (lane >= off) v += t;
+            }
+            if (x < side) {
+                const int rank = line_base + x * stride;
+                loads[(row + rank) * (2 * a.D) + port_plus + sgn] = (int64_t)(carry + v);
+            }
+            carry += __shfl(v, 63, 64);
+        }
+    }
+}
+
+}  // namespace
+}  // namespace trivance
+
+using trivance::CongArgs;
+
+extern "C" {
+
+int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topology* topo,
+                               int64_t* loads_dev, int64_t loads_len, void* stream) {
+    if (!plan) return TRIVANCE_EINVAL;
+    int routing = TRIVANCE_ROUTE_SCHEDULED;
+    if (topo) {
+        if (topo->ndims != plan->D) return TRIVANCE_EINVAL;
+        for (int d = 0; d < plan->D; ++d)
+            if (topo->dims[d] != plan->dims[d]) return TRIVANCE_EINVAL;
+        if (topo->routing != TRIVANCE_ROUTE_SCHEDULED && topo->routing != TRIVANCE_ROUTE_SHORTEST)
+            return TRIVANCE_EINVAL;
+        routing = topo->routing;
+    }
+    const int P = (int)plan->passes.size();
+    const int64_t need = (int64_t)P * plan->n * 2 * plan->D;
+    if (loads_len < need) return TRIVANCE_ESIZE;
+    if (need == 0) return TRIVANCE_OK;
+    if (!loads_dev) return TRIVANCE_EINVAL;
+    if (P > trivance::kMaxPasses) return TRIVANCE_EUNSUPPORTED;
+    const int side = plan->dims[0];
+    if (side > trivance::kMaxSide) return TRIVANCE_EUNSUPPORTED;
+
+    CongArgs a{};
+    a.n = plan->n;
+    a.D = plan->D;
+    a.npasses = P;
+    a.bruck = plan->variant == TRIVANCE_BRUCK_REF ? 1 : 0;
+    a.shortest = routing == TRIVANCE_ROUTE_SHORTEST ? 1 : 0;
+    a.lines = plan->n / side;
+    for (int d = 0; d < trivance::kMaxDims; ++d) {
+        a.dims[d] = d < plan->D ? plan->dims[d] : 1;
+        a.strides[d] = d < plan->D ? plan->strides[d] : 1;
+    }
+    for (int p = 0; p < P; ++p) {
+        a.distance[p] = plan->passes[p].distance;
+        for (int c = 0; c < trivance::kMaxDims; ++c) a.act_dim[p][c] = plan->passes[p].dim[c];
+    }
+    const uint32_t grid = (uint32_t)((int64_t)P * plan->D * a.lines);
+    const size_t lds = (size_t)(2 * side + 4) * sizeof(int);
+    hipLaunchKernelGGL(trivance::congestion_kernel, dim3(grid), dim3(64), lds,
+                       reinterpret_cast<hipStream_t>(stream), loads_dev, a);
+    return hipGetLastError() == hipSuccess ? TRIVANCE_OK : TRIVANCE_EHIP;
+}
+
+int64_t trivance_congestion(const trivance_plan_t* plan, const trivance_topology* topo,
+                            int64_t* loads, int64_t loads_len) {
+    if (!plan) return TRIVANCE_EINVAL;
+    const int64_t need = (int64_t)plan->passes.size() * plan->n * 2 * plan->D;
+    if (!loads) return need;
+    if (loads_len < need) return TRIVANCE_ESIZE;
+    if (need == 0) return TRIVANCE_OK;
+    int64_t* dev = nullptr;
+    if (hipMalloc(reinterpret_cast<void**>(&dev), need * sizeof(int64_t)) != hipSuccess)
+        return TRIVANCE_EHIP;
+    int rc = trivance_congestion_device(plan, topo, dev, need, nullptr);
+    if (rc == TRIVANCE_OK) {
+        if (hipMemcpy(loads, dev, need * sizeof(int64_t), hipMemcpyDeviceToHost) != hipSuccess)
+            rc = TRIVANCE_EHIP;
+    }
+    if (hipFree(dev) != hipSuccess && rc == TRIVANCE_OK) rc = TRIVANCE_EHIP;
+    return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,45 @@
+// Device-side input generator (not part of the AllReduce): counter-based U(-1, 1) fp32 values
+// from SplitMix64 (Steele, Lea, Flood, "Fast splittable pseudorandom number generators",
+// OOPSLA 2014). Value i of the rank-major array (i = r * elems + e) is the k-th output of a
+// SplitMix64 generator started at state 0, k = seed * 2^40 + i + 1: h = mix(k * golden_gamma);
+// the top 24 bits give u = (h >> 40) * 2^-23 - 1, exactly representable in fp32.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "plan.h"
+
+namespace trivance {
+namespace {
+
+__device__ __forceinline__ uint64_t splitmix64_mix(uint64_t z) {
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+__global__ __launch_bounds__(256) void fill_hash_uniform_kernel(float* __restrict__ out,
+                                                                uint64_t total, uint64_t key0) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const uint64_t h = splitmix64_mix((key0 + i + 1) * 0x9E3779B97F4A7C15ull);
+        out[i] = (float)(uint32_t)(h >> 40) * 0x1p-23f - 1.0f;
+    }
+}
+
+}  // namespace
+}  // namespace trivance
+
+extern "C" int trivance_fill_hash_uniform(void* buffers, int n, int64_t elems, uint64_t seed,
+                                          void* stream) {
+    if (n < 0 || elems < 0) return TRIVANCE_EINVAL;
+    const uint64_t total = (uint64_t)n * (uint64_t)elems;
+    if (total == 0) return TRIVANCE_OK;
+    if (!buffers) return TRIVANCE_EINVAL;
+    uint64_t blocks = (total + 255) / 256;
+    if (blocks > 65536ull * 8) blocks = 65536ull * 8;
+    hipLaunchKernelGGL(trivance::fill_hash_uniform_kernel, dim3((uint32_t)blocks), dim3(256), 0,
+                       reinterpret_cast<hipStream_t>(stream), static_cast<float*>(buffers), total,
+                       seed << 40);
+    return hipGetLastError() == hipSuccess ? TRIVANCE_OK : TRIVANCE_EHIP;
+}

@@ -1,0 +1,220 @@
+// Host-side schedule generator and byte accounting of the emulated Trivance AllReduce.
+//
+// Steps and peers: Sec. 4.1 (pi(r, k) = r -/+ 3^k), Theorem 1 (log3 n steps), Sec. 4.2 (the
+// latency-optimal variant uses the same pattern), Sec. 5 (one collective per torus dimension on
+// 1/D of the data, switching dimension every step; Appendix B's index t = d + D k fixes the
+// per-dimension step k = t div D). Block sets: the closed form of Sec. 4.3 says that the blocks
+// forwarded to peer p at step k are p + sum_{i>k} e_i 3^i; equivalently the blocks a rank keeps
+// after step k are those congruent to it modulo 3^(k+1). On a torus that congruence holds per
+// dimension, with the exponent counting the steps taken so far in that dimension.
+#include <cstdlib>
+#include <new>
+
+#include "plan.h"
+
+using trivance::kGranule;
+using trivance::kMaxDims;
+using trivance::Pass;
+
+namespace {
+
+int log3_exact(int v) {
+    int s = 0;
+    long long m = 1;
+    while (m < v) {
+        m *= 3;
+        ++s;
+    }
+    return m == v ? s : -1;
+}
+
+int ipow3(int e) {
+    int v = 1;
+    for (int i = 0; i < e; ++i) v *= 3;
+    return v;
+}
+
+// Fill the per-dimension moduli that hold after global step t for collective c.
+void fill_moduli(const trivance_plan_t* p, int t, int c, int* out) {
+    int count[kMaxDims] = {};
+    for (int s = 0; s <= t; ++s) count[(c + s) % p->D] += 1;
+    for (int d = 0; d < kMaxDims; ++d) out[d] = d < p->D ? ipow3(count[d]) : 1;
+}
+
+Pass make_pass(const trivance_plan_t* p, int phase, int t) {
+    Pass ps{};
+    ps.phase = phase;
+    ps.step = t;
+    ps.distance = ipow3(t / p->D);
+    for (int c = 0; c < kMaxDims; ++c) {
+        ps.dim[c] = c < p->D ? (c + t) % p->D : 0;
+        if (c < p->D) fill_moduli(p, t, c, ps.modulus[c]);
+    }
+    ps.kept_per_rank = p->n / ipow3(t + 1);
+    return ps;
+}
+
+}  // namespace
+
+namespace trivance {
+
+void block_bounds(const trivance_plan_t* p, int64_t elems, int c, int block, int64_t* begin,
+                  int64_t* end) {
+    const int64_t G = (elems + kGranule - 1) / kGranule;
+    const int64_t g0 = (int64_t)c * G / p->D;
+    const int64_t g1 = (int64_t)(c + 1) * G / p->D;
+    int64_t b = g0, e = g1;
+    if (block >= 0) {
+        const int64_t Gc = g1 - g0;
+        b = g0 + (int64_t)block * Gc / p->n;
+        e = g0 + (int64_t)(block + 1) * Gc / p->n;
+    }
+    *begin = b * kGranule < elems ? b * kGranule : elems;
+    *end = e * kGranule < elems ? e * kGranule : elems;
+}
+
+int64_t max_block_granules(const trivance_plan_t* p, int64_t elems) {
+    const int64_t G = (elems + kGranule - 1) / kGranule;
+    int64_t best = 0;
+    for (int c = 0; c < p->D; ++c) {
+        const int64_t Gc = (int64_t)(c + 1) * G / p->D - (int64_t)c * G / p->D;
+        const int64_t m = (Gc + p->n - 1) / p->n;  // ceil: the largest floor-difference
+        if (m > best) best = m;
+    }
+    return best;
+}
+
+}  // namespace trivance
+
+extern "C" {
+
+int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance_plan_t** out) {
+    if (!out) return TRIVANCE_EINVAL;
+    *out = nullptr;
+    if (n < 1 || ndims < 0) return TRIVANCE_EINVAL;
+    if (variant < TRIVANCE_LATENCY_OPT || variant > TRIVANCE_BRUCK_REF) return TRIVANCE_EINVAL;
+    int dims[kMaxDims] = {};
+    int D = ndims;
+    if (ndims == 0 || torus_dims == nullptr) {
+        D = 1;
+        dims[0] = n;
+    } else {
+        if (ndims > kMaxDims) return TRIVANCE_EUNSUPPORTED;
+        long long prod = 1;
+        for (int d = 0; d < ndims; ++d) {
+            if (torus_dims[d] < 1) return TRIVANCE_EINVAL;
+            dims[d] = torus_dims[d];
+            prod *= dims[d];
+            if (prod > (1LL << 30)) return TRIVANCE_EINVAL;
+        }
+        if (prod != n) return TRIVANCE_EINVAL;
+    }
+    for (int d = 0; d < D; ++d) {
+        if (log3_exact(dims[d]) < 0) return TRIVANCE_EUNSUPPORTED;
+        if (dims[d] != dims[0]) return TRIVANCE_EUNSUPPORTED;
+    }
+    if (variant == TRIVANCE_BRUCK_REF && D != 1) return TRIVANCE_EUNSUPPORTED;
+
+    trivance_plan_t* p = new (std::nothrow) trivance_plan_t;
+    if (!p) return TRIVANCE_ENOMEM;
+    p->n = n;
+    p->D = D;
+    p->variant = variant;
+    int stride = 1;
+    for (int d = 0; d < D; ++d) {
+        p->dims[d] = dims[d];
+        p->strides[d] = stride;
+        stride *= dims[d];
+        p->S += log3_exact(dims[d]);
+    }
+    try {
+        if (variant == TRIVANCE_BANDWIDTH_OPT) {
+            for (int t = 0; t < p->S; ++t)
+                p->passes.push_back(make_pass(p, TRIVANCE_PHASE_REDUCE_SCATTER, t));
+            for (int t = p->S - 1; t >= 0; --t)
+                p->passes.push_back(make_pass(p, TRIVANCE_PHASE_ALLGATHER, t));
+        } else {
+            for (int t = 0; t < p->S; ++t)
+                p->passes.push_back(make_pass(p, TRIVANCE_PHASE_LATENCY, t));
+        }
+    } catch (const std::bad_alloc&) {
+        delete p;
+        return TRIVANCE_ENOMEM;
+    }
+    *out = p;
+    return TRIVANCE_OK;
+}
+
+void trivance_plan_destroy(trivance_plan_t* plan) { delete plan; }
+
+int trivance_plan_num_steps(const trivance_plan_t* plan) {
+    return plan ? plan->S : TRIVANCE_EINVAL;
+}
+
+int trivance_plan_num_passes(const trivance_plan_t* plan) {
+    return plan ? (int)plan->passes.size() : TRIVANCE_EINVAL;
+}
+
+int trivance_plan_step(const trivance_plan_t* plan, int pass, int collective, int* phase,
+                       int* step, int* dim, int* distance) {
+    if (!plan || pass < 0 || pass >= (int)plan->passes.size() || collective < 0 ||
+        collective >= plan->D)
+        return TRIVANCE_EINVAL;
+    const Pass& ps = plan->passes[pass];
+    if (phase) *phase = ps.phase;
+    if (step) *step = ps.step;
+    if (dim) *dim = ps.dim[collective];
+    if (distance) *distance = ps.distance;
+    return TRIVANCE_OK;
+}
+
+int trivance_block_range(const trivance_plan_t* plan, int64_t elems, int collective, int block,
+                         int64_t* begin, int64_t* end) {
+    if (!plan || !begin || !end || elems < 0 || collective < 0 || collective >= plan->D ||
+        block < -1 || block >= plan->n)
+        return TRIVANCE_EINVAL;
+    trivance::block_bounds(plan, elems, collective, block, begin, end);
+    return TRIVANCE_OK;
+}
+
+int64_t trivance_pass_bytes(const trivance_plan_t* plan, int64_t elems, int dtype, int pass) {
+    if (!plan || elems < 0 || pass < 0 || pass >= (int)plan->passes.size()) return TRIVANCE_EINVAL;
+    if (dtype != TRIVANCE_F32 && dtype != TRIVANCE_I32) return TRIVANCE_EINVAL;
+    const int64_t w = 4;
+    const Pass& ps = plan->passes[pass];
+    const int64_t n = plan->n;
+    if (ps.phase == TRIVANCE_PHASE_LATENCY) return 2 * n * elems * w;
+    // Every (centre rank r, kept block j) pair of the pass touches block j in three rows:
+    // reduce-scatter reads own/left/right and writes own (4 accesses); all-gather reads the
+    // centre and writes both peers (3 accesses). Each block index j has exactly n / 3^(t+1)
+    // centres, and the blocks of all segments add up to the whole vector, so the pairs cover
+    // kept_per_rank * elems elements.
+    const int64_t covered = ps.kept_per_rank * elems;
+    const int64_t accesses = ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER ? 4 : 3;
+    return accesses * covered * w;
+}
+
+int64_t trivance_algorithmic_bytes(const trivance_plan_t* plan, int64_t elems, int dtype) {
+    if (!plan) return TRIVANCE_EINVAL;
+    int64_t total = 0;
+    for (int p = 0; p < (int)plan->passes.size(); ++p) {
+        const int64_t b = trivance_pass_bytes(plan, elems, dtype, p);
+        if (b < 0) return b;
+        total += b;
+    }
+    return total;
+}
+
+const char* trivance_strerror(int status) {
+    switch (status) {
+        case TRIVANCE_OK: return "success";
+        case TRIVANCE_EINVAL: return "invalid argument";
+        case TRIVANCE_EUNSUPPORTED: return "unsupported configuration";
+        case TRIVANCE_EHIP: return "HIP runtime error";
+        case TRIVANCE_ENOMEM: return "out of host memory";
+        case TRIVANCE_ESIZE: return "output buffer too small";
+        default: return "unknown status";
+    }
+}
+
+}  // extern "C"

@@ -1,0 +1,132 @@
+"""The C ABI without a GPU: the library loads, exports what include/trivance.h declares, and its
+host-side schedule logic agrees with the oracle (CPU only; no kernel is launched)."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2602_17254_amd as T
+from oracle import partition, schedule
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    if not os.path.exists(T.binding.LIB_PATH):
+        import __graft_entry__
+
+        __graft_entry__.build()
+    yield
+
+
+def test_exports_every_declared_symbol():
+    with open(os.path.join(ROOT, "include", "trivance.h")) as f:
+        header = f.read()
+    declared = set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]+?\b(trivance_\w+)\s*\(", header, re.M))
+    assert len(declared) >= 14
+    lib = ctypes.CDLL(T.binding.LIB_PATH)
+    missing = [s for s in sorted(declared) if not hasattr(lib, s)]
+    assert not missing, missing
+    assert set(T.binding.exported_symbols()) == declared
+
+
+@pytest.mark.parametrize("dims,variant", [((1,), "L"), ((3,), "B"), ((9,), "L"), ((81,), "L"),
+                                          ((243,), "B"), ((27, 27), "B"), ((9, 9, 9), "B"),
+                                          ((27, 27), "L"), ((9, 9, 9), "L"), ((81,), "BRUCK")])
+def test_plan_matches_oracle_schedule(dims, variant):
+    p = T.trivance_plan(dims, variant)
+    t = schedule.Torus(dims)
+    assert p.num_steps == t.steps
+    plist = schedule.pass_list(t, "L" if variant == "BRUCK" else variant)
+    assert p.num_passes == len(plist)
+    phase_code = {"L": T.binding.PHASE_LATENCY, "RS": T.binding.PHASE_REDUCE_SCATTER,
+                  "AG": T.binding.PHASE_ALLGATHER}
+    for i, (ph, step) in enumerate(plist):
+        for c in range(t.D):
+            got = T.trivance_plan_step(p, i, c)
+            dim, dist = schedule.step_dim_and_distance(t, c, step)
+            assert got == (phase_code[ph], step, dim, dist)
+
+
+@pytest.mark.parametrize("E,dims", [(0, (9,)), (1, (9,)), (1000, (27,)), (64 * 243 * 3 + 17, (243,)),
+                                    (1_048_576, (27, 27)), (33_554_432, (9, 9, 9)), (12345, (3, 3, 3))])
+def test_block_range_matches_oracle_partition(E, dims):
+    p = T.trivance_plan(dims, "B")
+    n, D = p.n, p.D
+    bb = partition.block_bounds(E, D, n)
+    js = range(n) if n <= 81 else list(range(0, n, 7)) + [n - 1]
+    for c in range(D):
+        assert T.trivance_block_range(p, E, c, -1) == partition.segment_bounds(E, D)[c]
+        for j in js:
+            assert T.trivance_block_range(p, E, c, j) == bb[c][j]
+
+
+@pytest.mark.parametrize("dims", [(9,), (81,), (243,), (27, 27), (9, 9, 9)])
+def test_algorithmic_bytes(dims):
+    """L: 2 S n E w per AllReduce; B: reduce-scatter step t reads n E w / 3^t and writes a third of
+    it, all-gather step t reads n E w / 3^(t+1) and writes twice that: 3.5 w E (n - 1) in total
+    (Sec. 7's reduction volume 1.5 m (1 - 1/n) per rank is the reduce-scatter read volume)."""
+    n = int(np.prod(dims))
+    S = schedule.Torus(dims).steps
+    for E in (0, 1, 4096, 33_554_432):
+        pl = T.trivance_plan(dims, "L")
+        assert T.trivance_algorithmic_bytes(pl, E) == 2 * S * n * E * 4
+        pb = T.trivance_plan(dims, "B")
+        assert 2 * T.trivance_algorithmic_bytes(pb, E) == 7 * 4 * E * (n - 1)
+        rs_reads = sum(3 * T.trivance_pass_bytes(pb, E, t) // 4 for t in range(S))
+        assert 2 * rs_reads == 3 * 4 * E * (n - 1)  # 1.5 m (1 - 1/n) per rank, times n ranks
+
+
+def test_plan_errors():
+    with pytest.raises(T.TrivanceError) as e:
+        T.trivance_plan((8,), "L")
+    assert e.value.status == -2
+    with pytest.raises(T.TrivanceError) as e:
+        T.trivance_plan((9, 27), "B")
+    assert e.value.status == -2
+    with pytest.raises(T.TrivanceError) as e:
+        T.trivance_plan((9, 9), "BRUCK")
+    assert e.value.status == -2
+    lib = T.binding._lib()
+    h = ctypes.c_void_p()
+    dims = (ctypes.c_int * 2)(9, 9)
+    assert lib.trivance_plan(80, dims, 2, 0, ctypes.byref(h)) == -1
+    assert lib.trivance_plan(0, None, 0, 0, ctypes.byref(h)) == -1
+    assert lib.trivance_plan(9, None, 0, 7, ctypes.byref(h)) == -1
+    assert lib.trivance_plan(9, None, 0, 0, None) == -1
+    p = T.trivance_plan((9,), "L")
+    with pytest.raises(T.TrivanceError):
+        T.trivance_plan_step(p, 2, 0)
+    with pytest.raises(T.TrivanceError):
+        T.trivance_block_range(p, 100, 1, 0)
+    assert lib.trivance_strerror(-5) == b"output buffer too small"
+
+
+def test_congestion_length_query_and_size_check():
+    """loads == NULL returns the required length; a short array is rejected before any GPU work."""
+    lib = T.binding._lib()
+    p = T.trivance_plan((27, 27), "B")
+    need = lib.trivance_congestion(p.handle, None, None, 0)
+    assert need == 12 * 729 * 4
+    buf = np.zeros(need - 1, dtype=np.int64)
+    rc = lib.trivance_congestion(p.handle, None, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                 need - 1)
+    assert rc == -5
+
+
+def test_executor_argument_checks_without_gpu():
+    """Argument validation happens before any HIP call: these return errors on a CPU-only host."""
+    lib = T.binding._lib()
+    p = T.trivance_plan((9,), "L")
+    assert lib.trivance_allreduce_emulated(None, 9, 100, 0, p.handle, None) == -1  # NULL buffers
+    assert lib.trivance_allreduce_emulated(None, 8, 100, 0, p.handle, None) == -1  # n mismatch
+    assert lib.trivance_allreduce_emulated(None, 9, -1, 0, p.handle, None) == -1
+    assert lib.trivance_allreduce_emulated(None, 9, 100, 5, p.handle, None) == -1  # dtype
+    assert lib.trivance_allreduce_emulated(None, 9, 0, 0, p.handle, None) == 0     # no-op
+    assert lib.trivance_allreduce_emulated_steps(None, 9, 10, 0, p.handle, None, 1, 3) == -1
+    b = T.trivance_plan((9,), "BRUCK")
+    assert lib.trivance_allreduce_emulated(None, 9, 10, 0, b.handle, None) == -2
