@@ -35,7 +35,11 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # HBM traffic per launch measured with rocprofv3 --pmc (FETCH_SIZE / WRITE_SIZE, scaled by the
 # same counters read for a plain copy of known size), keyed by kernel, valid only for the kernel
 # source it was measured on (sha256 of the source file, first 16 hex digits).
-MEASURED_TRAFFIC = {}
+MEASURED_TRAFFIC = {
+    # profiles/latency_split_kernel_ring81_8MiB_counters.md
+    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "24fc199ea8a73d39",
+                                                 "bytes_per_launch": 1359036216},
+}
 
 
 def _src_sha(path):
@@ -119,7 +123,9 @@ def run_workload(w, steps, warmup, with_cpu):
     del V_host
     T.trivance_allreduce_emulated(buf, plan)
     torch.cuda.synchronize()
-    first_cols = buf.index_select(1, torch.from_numpy(cols).cuda()).cpu().numpy()
+    first_cols = None
+    if with_cpu:
+        first_cols = buf.index_select(1, torch.from_numpy(cols).cuda()).cpu().numpy()
 
     # ---- warmup ----
     for _ in range(warmup):
@@ -146,7 +152,7 @@ def run_workload(w, steps, warmup, with_cpu):
 
     # dominant kernel: the pass type with the most total time
     phases = [T.trivance_plan_step(plan, p)[0] for p in range(P)]
-    names = {0: "latency_step_kernel", 1: "block_step_kernel<reduce>", 2: "block_step_kernel<copy>"}
+    names = {0: "latency_split_kernel", 1: "block_step_kernel<reduce>", 2: "block_step_kernel<copy>"}
     tot = {}
     for p, ph in enumerate(phases):
         tot.setdefault(ph, [0.0, 0, 0])
@@ -210,6 +216,23 @@ def run_workload(w, steps, warmup, with_cpu):
     return line
 
 
+def copy_probe(nbytes: int, reps: int = 3) -> None:
+    """A plain device copy of known size (torch's copy kernel), used to calibrate the rocprofv3
+    FETCH_SIZE / WRITE_SIZE counters against known traffic. Prints one JSON line."""
+    import torch
+
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / reps
+    print(json.dumps({"copy_probe_bytes": nbytes, "reps": reps, "ms": round(dt * 1e3, 4),
+                      "GBps_read_plus_write": round(2 * nbytes / dt / 1e9, 1)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -218,11 +241,16 @@ def main():
     ap.add_argument("--workload", default=inputs.HEADLINE, choices=sorted(inputs.WORKLOADS))
     ap.add_argument("--all", action="store_true", help="every named workload, one line each")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures a single-GPU emulation of all virtual ranks; it runs on exactly "
               "one GPU (--gpus 1).", file=sys.stderr)
         sys.exit(2)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     names = list(inputs.WORKLOADS) if args.all else [args.workload]
     for name in names:
         line = run_workload(inputs.WORKLOADS[name], args.steps, args.warmup,

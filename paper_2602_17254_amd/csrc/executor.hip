@@ -37,6 +37,29 @@ namespace {
 constexpr int kBlockThreads = 256;
 constexpr int kWavesPerBlock = kBlockThreads / 64;
 
+// Division by a per-pass constant d via a precomputed multiplier: for 0 <= x < 2^31,
+// x / d == (x * mul) >> shift with shift = 31 + ceil(log2 d), mul = floor(2^shift / d) + 1
+// (Granlund and Montgomery, "Division by invariant integers using multiplication", PLDI 1994).
+struct FastDiv {
+    uint64_t mul;
+    uint32_t shift;
+    uint32_t d;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+    uint32_t l = 0;
+    while (((uint64_t)1 << l) < d) ++l;
+    FastDiv f;
+    f.d = d;
+    f.shift = 31 + l;
+    f.mul = (((uint64_t)1 << f.shift) / d) + 1;
+    return f;
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t x, const FastDiv& f) {
+    return (uint32_t)(((uint64_t)x * f.mul) >> f.shift);
+}
+
 struct StepArgs {
     int64_t elems;                 // elements per rank row
     int64_t seg_g[kMaxDims + 1];   // segment granule starts, seg_g[D] = total granules
@@ -55,7 +78,11 @@ struct StepArgs {
     int cpb;                       // chunks per block
     uint32_t units_per_coll;       // n * kept * cpb
     uint32_t total_units;          // D * units_per_coll
-    int narrow;                    // 1 if n * (granules per segment) < 2^32
+    int narrow;                    // 1 if n * (granules per segment + 1) < 2^31
+    FastDiv f_upc, f_cpb, f_kept, f_n;
+    FastDiv f_side[kMaxDims];
+    FastDiv f_mod[kMaxDims][kMaxDims];   // modulus[c][d]
+    FastDiv f_nq[kMaxDims][kMaxDims];    // dims[d] / modulus[c][d]
 };
 
 template <typename T, int N>
@@ -84,13 +111,36 @@ __device__ __forceinline__ Vec<T, N> joint(const Vec<T, N>& own, const Vec<T, N>
 }
 
 template <typename T, int N>
+using Native = T __attribute__((ext_vector_type(N)));
+
+// 16-byte (or element) load/store; NT selects the non-temporal (streaming) cache policy.
+template <typename T, int N, bool NT = false>
 __device__ __forceinline__ Vec<T, N> ld(const T* p) {
-    return *reinterpret_cast<const Vec<T, N>*>(p);
+    Vec<T, N> r;
+    if constexpr (N == 1) {
+        r.v[0] = NT ? __builtin_nontemporal_load(p) : *p;
+    } else {
+        const Native<T, N>* q = reinterpret_cast<const Native<T, N>*>(p);
+        const Native<T, N> x = NT ? __builtin_nontemporal_load(q) : *q;
+#pragma unroll
+        for (int i = 0; i < N; ++i) r.v[i] = x[i];
+    }
+    return r;
 }
 
-template <typename T, int N>
+template <typename T, int N, bool NT = false>
 __device__ __forceinline__ void st(T* p, const Vec<T, N>& v) {
-    *reinterpret_cast<Vec<T, N>*>(p) = v;
+    if constexpr (N == 1) {
+        if (NT) __builtin_nontemporal_store(v.v[0], p);
+        else *p = v.v[0];
+    } else {
+        Native<T, N> x;
+#pragma unroll
+        for (int i = 0; i < N; ++i) x[i] = v.v[i];
+        Native<T, N>* q = reinterpret_cast<Native<T, N>*>(p);
+        if (NT) __builtin_nontemporal_store(x, q);
+        else *q = x;
+    }
 }
 
 __device__ __forceinline__ int64_t imin64(int64_t a, int64_t b) { return a < b ? a : b; }
@@ -181,6 +231,74 @@ __global__ __launch_bounds__(kBlockThreads) void latency_step_kernel(T* __restri
 }
 
 // ---------------------------------------------------------------------------------------------
+// Latency-optimal step, cycle of LEN = P * SUB ranks split over the P wavefronts of a workgroup.
+// Wave w walks rows [w SUB, (w+1) SUB) of the cycle for 64 column vectors. The only values a
+// wave needs from outside its rows are the pre-step rows just before and after its range; every
+// wave publishes its own first and last row in LDS and reads its neighbours' after one barrier,
+// before any store, so the in-place update stays correct. Splitting gives P times more, P times
+// shorter wavefronts than walking the whole cycle in one wavefront.
+template <typename T, int VEC, int SUB, int P, int PD, bool NT>
+__global__ __launch_bounds__(64 * P) void latency_split_kernel(T* __restrict__ buf, StepArgs a) {
+    static_assert(SUB % 3 == 0, "rows are processed in groups of three");
+    using V = Vec<T, VEC>;
+    constexpr int G = SUB / 3;
+    __shared__ V halo[P][2][64];
+
+    const uint32_t wg = blockIdx.x;
+    const uint32_t cb = wg % (uint32_t)a.colblocks;
+    const uint32_t rest = wg / (uint32_t)a.colblocks;
+    const int cyc = (int)(rest % (uint32_t)a.ncycles);
+    const int c = (int)(rest / (uint32_t)a.ncycles);
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+
+    const int dim = a.act_dim[c];
+    const int side = a.dims[dim];
+    const int stride = a.strides[dim];
+    const int dist = a.distance;
+    const int res = cyc % dist;
+    const int other = cyc / dist;
+    const int first_rank = (other % stride) + (other / stride) * stride * side + res * stride;
+
+    const int64_t E = a.elems;
+    const int64_t seg_b = imin64(a.seg_g[c] * kGranule, E);
+    const int64_t seg_e = imin64(a.seg_g[c + 1] * kGranule, E);
+    const int64_t nvec = (seg_e - seg_b) / VEC;
+    const int64_t v_idx = (int64_t)cb * 64 + lane;
+    const bool ok = v_idx < nvec;
+    const int64_t rowstep = (int64_t)dist * stride * E;
+    T* const col = buf + (int64_t)first_rank * E + seg_b + (ok ? v_idx : 0) * VEC +
+                   (int64_t)(w * SUB) * rowstep;
+
+    V v[SUB];
+    if (ok) {
+        v[0] = ld<T, VEC, NT>(col);
+        v[SUB - 1] = ld<T, VEC, NT>(col + (int64_t)(SUB - 1) * rowstep);
+#pragma unroll
+        for (int i = 1; i < 3 * (PD + 1); ++i)
+            if (i < SUB - 1) v[i] = ld<T, VEC, NT>(col + (int64_t)i * rowstep);
+        halo[w][0][lane] = v[0];
+        halo[w][1][lane] = v[SUB - 1];
+    }
+    __syncthreads();
+    if (!ok) return;
+    const V before = halo[(w + P - 1) % P][1][lane];  // pre-step row w SUB - 1
+    const V after = halo[(w + 1) % P][0][lane];       // pre-step row (w + 1) SUB
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+#pragma unroll
+        for (int i = 3 * (g + PD + 1); i < 3 * (g + PD + 2); ++i)
+            if (i < SUB - 1) v[i] = ld<T, VEC, NT>(col + (int64_t)i * rowstep);
+#pragma unroll
+        for (int i = 3 * g; i < 3 * g + 3; ++i) {
+            const V& left = i == 0 ? before : v[i > 0 ? i - 1 : 0];
+            const V& right = i == SUB - 1 ? after : v[i + 1 < SUB ? i + 1 : i];
+            st<T, VEC, NT>(col + (int64_t)i * rowstep, joint(v[i], left, right));
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------------------
 // Decode of a block-step work unit (all values wave-uniform).
 struct Unit {
     int64_t begin, end;  // element range of this unit's chunk (begin < end when active)
@@ -189,42 +307,44 @@ struct Unit {
 
 __device__ __forceinline__ bool decode_unit(const StepArgs& a, uint32_t unit, int chunk_elems,
                                             Unit* out) {
-    const uint32_t c = unit / a.units_per_coll;
+    const uint32_t c = fdiv(unit, a.f_upc);
     const uint32_t rem = unit - c * a.units_per_coll;
-    const uint32_t pair = rem / (uint32_t)a.cpb;
-    const int chunk = (int)(rem - pair * (uint32_t)a.cpb);
-    const int r = (int)(pair / (uint32_t)a.kept);
-    int q = (int)(pair - (uint32_t)r * (uint32_t)a.kept);
+    const uint32_t pair = fdiv(rem, a.f_cpb);
+    const uint32_t chunk = rem - pair * (uint32_t)a.cpb;
+    const uint32_t r = fdiv(pair, a.f_kept);
+    uint32_t q = pair - r * (uint32_t)a.kept;
     const int act = a.act_dim[c];
 
-    int j = 0, rr = r, r_act = 0;
+    uint32_t j = 0, rr = r, r_act = 0;
 #pragma unroll
     for (int d = 0; d < kMaxDims; ++d) {
         if (d < a.D) {
-            const int side = a.dims[d];
-            const int rd = rr % side;
-            rr /= side;
-            const int K = a.modulus[c][d];
-            const int nq = side / K;
-            const int qd = q % nq;
-            q /= nq;
-            j += (rd % K + K * qd) * a.strides[d];
+            const uint32_t rr_next = fdiv(rr, a.f_side[d]);
+            const uint32_t rd = rr - rr_next * (uint32_t)a.dims[d];
+            rr = rr_next;
+            const FastDiv& fk = a.f_mod[c][d];
+            const FastDiv& fq = a.f_nq[c][d];
+            const uint32_t q_next = fdiv(q, fq);
+            const uint32_t qd = q - q_next * fq.d;
+            q = q_next;
+            const uint32_t rd_mod = rd - fdiv(rd, fk) * fk.d;
+            j += (rd_mod + fk.d * qd) * (uint32_t)a.strides[d];
             if (d == act) r_act = rd;
         }
     }
     const int side = a.dims[act];
     const int st = a.strides[act];
     const int dist = a.distance;
-    out->rank = r;
-    out->left = r_act >= dist ? r - dist * st : r + (side - dist) * st;
-    out->right = r_act + dist < side ? r + dist * st : r - (side - dist) * st;
+    out->rank = (int)r;
+    out->left = (int)r_act >= dist ? (int)r - dist * st : (int)r + (side - dist) * st;
+    out->right = (int)r_act + dist < side ? (int)r + dist * st : (int)r - (side - dist) * st;
 
     const int64_t g0 = a.seg_g[c];
     const int64_t Gc = a.seg_g[c + 1] - g0;
     int64_t gb, ge;
     if (a.narrow) {
-        gb = g0 + (int64_t)((uint32_t)j * (uint32_t)Gc / (uint32_t)a.n);
-        ge = g0 + (int64_t)((uint32_t)(j + 1) * (uint32_t)Gc / (uint32_t)a.n);
+        gb = g0 + fdiv(j * (uint32_t)Gc, a.f_n);
+        ge = g0 + fdiv((j + 1) * (uint32_t)Gc, a.f_n);
     } else {
         gb = g0 + (int64_t)j * Gc / a.n;
         ge = g0 + (int64_t)(j + 1) * Gc / a.n;
@@ -237,7 +357,7 @@ __device__ __forceinline__ bool decode_unit(const StepArgs& a, uint32_t unit, in
     return out->begin < e;
 }
 
-template <typename T, int VEC, int U, bool REDUCE>
+template <typename T, int VEC, int U, bool REDUCE, bool NT>
 __global__ __launch_bounds__(kBlockThreads) void block_step_kernel(T* __restrict__ buf,
                                                                    StepArgs a) {
     using V = Vec<T, VEC>;
@@ -265,24 +385,24 @@ __global__ __launch_bounds__(kBlockThreads) void block_step_kernel(T* __restrict
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (ok[u]) {
-                x[u] = ld<T, VEC>(own + idx[u]);
-                y[u] = ld<T, VEC>(pl + idx[u]);
-                z[u] = ld<T, VEC>(pr + idx[u]);
+                x[u] = ld<T, VEC, NT>(own + idx[u]);
+                y[u] = ld<T, VEC, NT>(pl + idx[u]);
+                z[u] = ld<T, VEC, NT>(pr + idx[u]);
             }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (ok[u]) st<T, VEC>(own + idx[u], joint(x[u], y[u], z[u]));
+            if (ok[u]) st<T, VEC, NT>(own + idx[u], joint(x[u], y[u], z[u]));
     } else {
         V x[U];
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (ok[u]) x[u] = ld<T, VEC>(own + idx[u]);
+            if (ok[u]) x[u] = ld<T, VEC, NT>(own + idx[u]);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (ok[u]) {
-                st<T, VEC>(pl + idx[u], x[u]);
-                st<T, VEC>(pr + idx[u], x[u]);
+                st<T, VEC, NT>(pl + idx[u], x[u]);
+                st<T, VEC, NT>(pr + idx[u], x[u]);
             }
         }
     }
@@ -291,64 +411,15 @@ __global__ __launch_bounds__(kBlockThreads) void block_step_kernel(T* __restrict
 // ---------------------------------------------------------------------------------------------
 // Host side.
 
-constexpr int kLatencyVPT = 1;
+// Launch geometry of one pass.
+struct Launch {
+    uint32_t grid = 0;
+    int U = 0;            // block steps: 16-byte vectors per lane per chunk
+    int64_t max_vec = 0;  // latency steps: column vectors of the longest segment
+};
 
-template <typename T, int VEC>
-hipError_t launch_pass(T* buf, const StepArgs& a0, int phase, int max_blk_elems,
-                       hipStream_t stream) {
-    StepArgs a = a0;
-    if (phase == TRIVANCE_PHASE_LATENCY) {
-        int64_t max_seg = 0;
-        for (int c = 0; c < a.D; ++c) {
-            const int64_t b = std::min(a.seg_g[c] * kGranule, a.elems);
-            const int64_t e = std::min(a.seg_g[c + 1] * kGranule, a.elems);
-            max_seg = std::max(max_seg, e - b);
-        }
-        const int64_t max_vec = (max_seg + VEC - 1) / VEC;
-        const int64_t per_block = (int64_t)kBlockThreads * kLatencyVPT;
-        a.colblocks = (int)((max_vec + per_block - 1) / per_block);
-        if (a.colblocks < 1) a.colblocks = 1;
-        const int64_t grid = (int64_t)a.D * a.ncycles * a.colblocks;
-        if (grid >= (int64_t)1 << 31) return hipErrorInvalidConfiguration;
-        hipLaunchKernelGGL((latency_step_kernel<T, VEC, kLatencyVPT>), dim3((uint32_t)grid),
-                           dim3(kBlockThreads), 0, stream, buf, a);
-        return hipGetLastError();
-    }
-    // chunk size: four 16-byte vectors per lane for large blocks, fewer for small ones
-    int U = 4;
-    if (max_blk_elems <= 64 * VEC) U = 1;
-    else if (max_blk_elems <= 2 * 64 * VEC) U = 2;
-    const int chunk = 64 * VEC * U;
-    a.cpb = (max_blk_elems + chunk - 1) / chunk;
-    if (a.cpb < 1) a.cpb = 1;
-    const int64_t upc = (int64_t)a.n * a.kept * a.cpb;
-    const int64_t total = upc * a.D;
-    if (total >= ((int64_t)1 << 32) - kWavesPerBlock) return hipErrorInvalidConfiguration;
-    a.units_per_coll = (uint32_t)upc;
-    a.total_units = (uint32_t)total;
-    const uint32_t grid = (uint32_t)((total + kWavesPerBlock - 1) / kWavesPerBlock);
-    const bool rs = phase == TRIVANCE_PHASE_REDUCE_SCATTER;
-#define TRIVANCE_LAUNCH_BLOCK(UU)                                                              \
-    if (rs)                                                                                    \
-        hipLaunchKernelGGL((block_step_kernel<T, VEC, UU, true>), dim3(grid),                  \
-                           dim3(kBlockThreads), 0, stream, buf, a);                            \
-    else                                                                                       \
-        hipLaunchKernelGGL((block_step_kernel<T, VEC, UU, false>), dim3(grid),                 \
-                           dim3(kBlockThreads), 0, stream, buf, a);
-    if (U == 4) {
-        TRIVANCE_LAUNCH_BLOCK(4)
-    } else if (U == 2) {
-        TRIVANCE_LAUNCH_BLOCK(2)
-    } else {
-        TRIVANCE_LAUNCH_BLOCK(1)
-    }
-#undef TRIVANCE_LAUNCH_BLOCK
-    return hipGetLastError();
-}
-
-template <typename T>
-int run_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
-               int pe) {
+// Arguments common to every pass of one call.
+inline int base_args(const trivance_plan_t* p, int64_t elems, StepArgs* out, int64_t* max_blk) {
     StepArgs a{};
     a.elems = elems;
     a.n = p->n;
@@ -361,27 +432,145 @@ int run_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stre
     }
     int64_t max_gc = 0;
     for (int c = 0; c < p->D; ++c) max_gc = std::max<int64_t>(max_gc, a.seg_g[c + 1] - a.seg_g[c]);
-    a.narrow = (int64_t)p->n * (max_gc + 1) < ((int64_t)1 << 32) ? 1 : 0;
-    const int64_t max_blk = max_block_granules(p, elems) * kGranule;
-    if (max_blk >= ((int64_t)1 << 31)) return TRIVANCE_EUNSUPPORTED;
+    a.narrow = (int64_t)p->n * (max_gc + 1) < ((int64_t)1 << 31) ? 1 : 0;
+    a.f_n = make_fastdiv((uint32_t)p->n);
+    for (int d = 0; d < kMaxDims; ++d) a.f_side[d] = make_fastdiv((uint32_t)a.dims[d]);
+    *max_blk = max_block_granules(p, elems) * kGranule;
+    if (*max_blk >= ((int64_t)1 << 31)) return TRIVANCE_EUNSUPPORTED;
+    *out = a;
+    return TRIVANCE_OK;
+}
 
-    const bool vec4 = (elems % 4 == 0) && ((uintptr_t)buf % 16 == 0);
+// Per-pass fields: active dimensions, distance, moduli and the launch geometry.
+template <int VEC>
+inline int pass_args(const trivance_plan_t* p, const Pass& ps, int64_t max_blk, int chunk_vecs,
+                     StepArgs* a, Launch* L) {
+    a->distance = ps.distance;
+    for (int c = 0; c < kMaxDims; ++c) {
+        a->act_dim[c] = ps.dim[c];
+        for (int d = 0; d < kMaxDims; ++d) {
+            const int m = c < p->D && d < p->D ? ps.modulus[c][d] : 1;
+            a->modulus[c][d] = m;
+            a->f_mod[c][d] = make_fastdiv((uint32_t)m);
+            a->f_nq[c][d] = make_fastdiv((uint32_t)(a->dims[d] / m));
+        }
+    }
+    const int side = p->dims[ps.dim[0]];
+    a->ncycles = (p->n / side) * ps.distance;
+    a->kept = (int)ps.kept_per_rank;
+    if (ps.phase == TRIVANCE_PHASE_LATENCY) {
+        int64_t max_seg = 0;
+        for (int c = 0; c < a->D; ++c) {
+            const int64_t b = std::min(a->seg_g[c] * kGranule, a->elems);
+            const int64_t e = std::min(a->seg_g[c + 1] * kGranule, a->elems);
+            max_seg = std::max(max_seg, e - b);
+        }
+        L->max_vec = (max_seg + VEC - 1) / VEC;
+        // grid for 64-column workgroups (the split-cycle kernel); the other latency kernels
+        // recompute it for 256 columns
+        a->colblocks = (int)std::max<int64_t>(1, (L->max_vec + 63) / 64);
+        const int64_t grid = (int64_t)a->D * a->ncycles * a->colblocks;
+        if (grid >= ((int64_t)1 << 31)) return TRIVANCE_EUNSUPPORTED;
+        L->grid = (uint32_t)grid;
+        return TRIVANCE_OK;
+    }
+    // chunk: U 16-byte vectors per lane. One (1 KiB of fp32 per row and wavefront) measured
+    // best on MI355X for every workload shape; larger chunks over-subscribe the memory system.
+    const int U = chunk_vecs;
+    const int64_t chunk = 64 * VEC * U;
+    a->cpb = (int)std::max<int64_t>(1, (max_blk + chunk - 1) / chunk);
+    const int64_t upc = (int64_t)a->n * a->kept * a->cpb;
+    const int64_t total = upc * a->D;
+    if (total >= ((int64_t)1 << 31) - kWavesPerBlock) return TRIVANCE_EUNSUPPORTED;
+    a->units_per_coll = (uint32_t)upc;
+    a->total_units = (uint32_t)total;
+    a->f_upc = make_fastdiv((uint32_t)upc);
+    a->f_cpb = make_fastdiv((uint32_t)a->cpb);
+    a->f_kept = make_fastdiv((uint32_t)a->kept);
+    L->grid = (uint32_t)((total + kWavesPerBlock - 1) / kWavesPerBlock);
+    L->U = U;
+    return TRIVANCE_OK;
+}
+
+// Re-derive the grid for workgroups covering `cols` column vectors each.
+inline void set_columns(StepArgs* a, Launch* L, int cols) {
+    a->colblocks = (int)std::max<int64_t>(1, (L->max_vec + cols - 1) / cols);
+    L->grid = (uint32_t)((int64_t)a->D * a->ncycles * a->colblocks);
+}
+
+template <typename T, int VEC, int SUB, int P>
+void launch_split(T* buf, StepArgs a, Launch L, hipStream_t stream) {
+    set_columns(&a, &L, 64);
+    hipLaunchKernelGGL((latency_split_kernel<T, VEC, SUB, P, 1, true>), dim3(L.grid),
+                       dim3(64 * P), 0, stream, buf, a);
+}
+
+template <typename T, int VEC>
+hipError_t launch_latency(T* buf, const StepArgs& a, const Launch& L, int len,
+                          hipStream_t stream) {
+    switch (len) {
+        // rows per wavefront x wavefronts per workgroup, measured best on MI355X
+        case 3: launch_split<T, VEC, 3, 1>(buf, a, L, stream); break;
+        case 9: launch_split<T, VEC, 3, 3>(buf, a, L, stream); break;
+        case 27: launch_split<T, VEC, 3, 9>(buf, a, L, stream); break;
+        case 81: launch_split<T, VEC, 9, 9>(buf, a, L, stream); break;
+        case 243: launch_split<T, VEC, 27, 9>(buf, a, L, stream); break;
+        default: {
+            StepArgs b = a;
+            Launch M = L;
+            set_columns(&b, &M, kBlockThreads);
+            hipLaunchKernelGGL((latency_step_kernel<T, VEC, 1>), dim3(M.grid),
+                               dim3(kBlockThreads), 0, stream, buf, b);
+            break;
+        }
+    }
+    return hipGetLastError();
+}
+
+template <typename T, int VEC>
+hipError_t launch_block(T* buf, const StepArgs& a, const Launch& L, bool reduce,
+                        hipStream_t stream) {
+    if (L.U != 1) return hipErrorInvalidValue;
+    const dim3 grid(L.grid), block(kBlockThreads);
+    if (reduce)
+        hipLaunchKernelGGL((block_step_kernel<T, VEC, 1, true, true>), grid, block, 0, stream,
+                           buf, a);
+    else
+        hipLaunchKernelGGL((block_step_kernel<T, VEC, 1, false, true>), grid, block, 0, stream,
+                           buf, a);
+    return hipGetLastError();
+}
+
+template <typename T, int VEC>
+int run_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
+                   int pe) {
+    StepArgs a;
+    int64_t max_blk;
+    int rc = base_args(p, elems, &a, &max_blk);
+    if (rc != TRIVANCE_OK) return rc;
     for (int pi = pb; pi < pe; ++pi) {
         const Pass& ps = p->passes[pi];
-        a.distance = ps.distance;
-        for (int c = 0; c < kMaxDims; ++c) {
-            a.act_dim[c] = ps.dim[c];
-            for (int d = 0; d < kMaxDims; ++d) a.modulus[c][d] = ps.modulus[c][d];
-        }
-        const int side = p->dims[ps.dim[0]];
-        a.ncycles = (p->n / side) * ps.distance;
-        a.kept = (int)ps.kept_per_rank;
-        const hipError_t err = vec4 ? launch_pass<T, 4>(buf, a, ps.phase, (int)max_blk, stream)
-                                    : launch_pass<T, 1>(buf, a, ps.phase, (int)max_blk, stream);
-        if (err == hipErrorInvalidConfiguration) return TRIVANCE_EUNSUPPORTED;
+        Launch L;
+        rc = pass_args<VEC>(p, ps, max_blk, 1, &a, &L);
+        if (rc != TRIVANCE_OK) return rc;
+        hipError_t err;
+        if (ps.phase == TRIVANCE_PHASE_LATENCY)
+            err = launch_latency<T, VEC>(buf, a, L, p->dims[ps.dim[0]] / ps.distance, stream);
+        else
+            err = launch_block<T, VEC>(buf, a, L, ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER,
+                                       stream);
         if (err != hipSuccess) return TRIVANCE_EHIP;
     }
     return TRIVANCE_OK;
+}
+
+template <typename T>
+int run_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
+               int pe) {
+    // 16-byte vectors need 16-byte aligned rows: an aligned base and elems % 4 == 0
+    if (elems % 4 == 0 && (uintptr_t)buf % 16 == 0)
+        return run_passes_vec<T, 4>(buf, elems, p, stream, pb, pe);
+    return run_passes_vec<T, 1>(buf, elems, p, stream, pb, pe);
 }
 
 }  // namespace
