@@ -36,9 +36,15 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # same counters read for a plain copy of known size), keyed by kernel, valid only for the kernel
 # source it was measured on (sha256 of the source file, first 16 hex digits).
 MEASURED_TRAFFIC = {
-    # profiles/latency_split_kernel_ring81_8MiB_counters.md
-    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "24fc199ea8a73d39",
-                                                 "bytes_per_launch": 1359036216},
+    # profiles/latency_split_kernel_ring81_L_8MiB.md, profiles/block_step_kernel_*.md
+    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "3ee85e63946bf549",
+                                                 "bytes_per_launch": 1359030905},
+    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "3ee85e63946bf549",
+                                                        "bytes_per_launch": 3248087063},
+    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "3ee85e63946bf549",
+                                                          "bytes_per_launch": 1017882172},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "3ee85e63946bf549",
+                                                            "bytes_per_launch": 32569549948},
 }
 
 

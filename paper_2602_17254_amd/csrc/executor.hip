@@ -145,6 +145,16 @@ __device__ __forceinline__ void st(T* p, const Vec<T, N>& v) {
 
 __device__ __forceinline__ int64_t imin64(int64_t a, int64_t b) { return a < b ? a : b; }
 
+// Workgroup index remapped so that each of the 8 XCDs (which receive workgroups round-robin)
+// works on one contiguous range of units.
+__device__ __forceinline__ uint32_t xcd_contiguous(uint32_t wg, uint32_t nwg) {
+    constexpr uint32_t kXcds = 8;
+    const uint32_t per = nwg / kXcds, rem = nwg % kXcds;
+    const uint32_t xcd = wg % kXcds, idx = wg / kXcds;
+    return xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+}
+
+
 // ---------------------------------------------------------------------------------------------
 // Latency-optimal step: sliding window over one rank cycle.
 // Grid: D * ncycles * colblocks thread blocks; each thread owns VPT column vectors.
@@ -237,14 +247,14 @@ __global__ __launch_bounds__(kBlockThreads) void latency_step_kernel(T* __restri
 // wave publishes its own first and last row in LDS and reads its neighbours' after one barrier,
 // before any store, so the in-place update stays correct. Splitting gives P times more, P times
 // shorter wavefronts than walking the whole cycle in one wavefront.
-template <typename T, int VEC, int SUB, int P, int PD, bool NT>
+template <typename T, int VEC, int SUB, int P, int PD, bool NT, bool XCD = false>
 __global__ __launch_bounds__(64 * P) void latency_split_kernel(T* __restrict__ buf, StepArgs a) {
     static_assert(SUB % 3 == 0, "rows are processed in groups of three");
     using V = Vec<T, VEC>;
     constexpr int G = SUB / 3;
     __shared__ V halo[P][2][64];
 
-    const uint32_t wg = blockIdx.x;
+    const uint32_t wg = XCD ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x;
     const uint32_t cb = wg % (uint32_t)a.colblocks;
     const uint32_t rest = wg / (uint32_t)a.colblocks;
     const int cyc = (int)(rest % (uint32_t)a.ncycles);
@@ -357,14 +367,15 @@ __device__ __forceinline__ bool decode_unit(const StepArgs& a, uint32_t unit, in
     return out->begin < e;
 }
 
-template <typename T, int VEC, int U, bool REDUCE, bool NT>
+template <typename T, int VEC, int U, bool REDUCE, bool NT, bool XCD = false>
 __global__ __launch_bounds__(kBlockThreads) void block_step_kernel(T* __restrict__ buf,
                                                                    StepArgs a) {
     using V = Vec<T, VEC>;
     constexpr int kChunk = 64 * VEC * U;
     const int lane = threadIdx.x & 63;
     const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const uint32_t unit = blockIdx.x * (uint32_t)kWavesPerBlock + wave;
+    const uint32_t wg = XCD ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x;
+    const uint32_t unit = wg * (uint32_t)kWavesPerBlock + wave;
     if (unit >= a.total_units) return;
     Unit w;
     if (!decode_unit(a, unit, kChunk, &w)) return;
@@ -533,11 +544,11 @@ hipError_t launch_block(T* buf, const StepArgs& a, const Launch& L, bool reduce,
     if (L.U != 1) return hipErrorInvalidValue;
     const dim3 grid(L.grid), block(kBlockThreads);
     if (reduce)
-        hipLaunchKernelGGL((block_step_kernel<T, VEC, 1, true, true>), grid, block, 0, stream,
-                           buf, a);
+        hipLaunchKernelGGL((block_step_kernel<T, VEC, 1, true, true, true>), grid, block, 0,
+                           stream, buf, a);
     else
-        hipLaunchKernelGGL((block_step_kernel<T, VEC, 1, false, true>), grid, block, 0, stream,
-                           buf, a);
+        hipLaunchKernelGGL((block_step_kernel<T, VEC, 1, false, true, true>), grid, block, 0,
+                           stream, buf, a);
     return hipGetLastError();
 }
 
