@@ -239,6 +239,45 @@ def copy_probe(nbytes: int, reps: int = 3) -> None:
                       "GBps_read_plus_write": round(2 * nbytes / dt / 1e9, 1)}), flush=True)
 
 
+SWEEP_CLASSES = [((81,), "L"), ((243,), "B"), ((27, 27), "B"), ((9, 9, 9), "B")]
+SWEEP_MIB = [8, 16, 32, 64, 128]
+
+
+def sweep(steps: int, warmup: int) -> None:
+    """Throughput of each topology/variant class at 8..128 MiB per rank (one JSON line each).
+    Inputs are the device-generated U(-1, 1) values; correctness is covered by the test suite."""
+    import torch
+
+    import paper_2602_17254_amd as T
+
+    torch.cuda.set_device(0)
+    for dims, variant in SWEEP_CLASSES:
+        plan = T.trivance_plan(dims, variant)
+        n = plan.n
+        for mib in SWEEP_MIB:
+            E = mib * 2 ** 20 // 4
+            _say(f"[sweep] {'x'.join(map(str, dims))} {variant} {mib} MiB per rank")
+            buf = torch.empty((n, E), dtype=torch.float32, device="cuda")
+            T.trivance_fill_hash_uniform(buf, 7)
+            for _ in range(warmup):
+                T.trivance_allreduce_emulated(buf, plan)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                T.trivance_allreduce_emulated(buf, plan)
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) * 1e3 / steps
+            alg = T.trivance_algorithmic_bytes(plan, E)
+            gbps = alg / (ms * 1e-3) / 1e9
+            print(json.dumps({"sweep": "x".join(map(str, dims)), "variant": variant,
+                              "rank_mib": mib, "n_ranks": n, "passes": plan.num_passes,
+                              "ms_per_allreduce": round(ms, 4), "GBps": round(gbps, 1),
+                              "pct_of_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
+                              "resident_GB": round(n * E * 4 / 1e9, 2)}), flush=True)
+            del buf
+            torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -247,6 +286,8 @@ def main():
     ap.add_argument("--workload", default=inputs.HEADLINE, choices=sorted(inputs.WORKLOADS))
     ap.add_argument("--all", action="store_true", help="every named workload, one line each")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="8..128 MiB per rank for every topology/variant class")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES (counter calibration)")
     args = ap.parse_args()
@@ -256,6 +297,9 @@ def main():
         sys.exit(2)
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.sweep:
+        sweep(args.steps, args.warmup)
         return
     names = list(inputs.WORKLOADS) if args.all else [args.workload]
     for name in names:
