@@ -80,12 +80,15 @@ typedef enum {
  * Schedule (Sec. 4.1 peers pi(r,k) = r -/+ 3^k; Theorem 1 step count; Sec. 5 tori): S = log3(n)
  * steps. On a D-dimensional torus D collectives run concurrently, collective c on segment c of
  * every vector; at global step t collective c works on dimension (c + t) mod D at distance
- * 3^(t div D) (Sec. 5 dimension switching, Appendix B step index t = d + D k).
+ * 3^(t div D) (Sec. 5 dimension switching, Appendix B step index t = d + D k). Sides may differ
+ * (rectangular tori, which Sec. 5 does not cover); then collective c at step t takes the first
+ * dimension, in cyclic order from (c + t) mod D, in which it still has steps left, at distance
+ * 3^(steps it already took there). With equal sides both rules coincide.
  *
  * Errors: EINVAL for out == NULL, n < 1, ndims < 0, a side < 1, product != n;
  *         EUNSUPPORTED for a side that is not a power of three (Sec. 4.4's final-step rule is not
- *         implemented), unequal sides (no rotation rule in the paper), ndims > TRIVANCE_MAX_DIMS,
- *         or TRIVANCE_BRUCK_REF on more than one dimension.
+ *         implemented), ndims > TRIVANCE_MAX_DIMS, or TRIVANCE_BRUCK_REF on more than one
+ *         dimension.
  */
 int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance_plan_t** out);
 
@@ -104,7 +107,7 @@ int trivance_plan_num_passes(const trivance_plan_t* plan);
  *   phase    <- a trivance_phase
  *   step     <- global step index t (all-gather passes run t = S-1 .. 0)
  *   dim      <- torus dimension used by this collective in this pass
- *   distance <- peer distance 3^(t div D)
+ *   distance <- peer distance of this collective in this pass (3^(t div D) for equal sides)
  * Any output pointer may be NULL. EINVAL if pass or collective is out of range.
  */
 int trivance_plan_step(const trivance_plan_t* plan, int pass, int collective, int* phase,

@@ -15,6 +15,11 @@ Sources in the paper:
 
 Rank numbering on a torus (a reading; the paper does not fix one): rank = sum_d x_d * stride_d,
 dimension 0 fastest. Block j of a collective's segment is owned by rank j (Sec. 4.1 generalised).
+
+Unequal sides (rectangular tori) are outside Sec. 5. Reading used for them: collective c at global
+step t takes the first dimension, in cyclic order starting at (c + t) mod D, in which it still has
+steps left; its distance there is 3^(steps it already took in that dimension). With equal sides
+this is the rule above.
 """
 
 from __future__ import annotations
@@ -48,10 +53,6 @@ class Torus:
             raise ValueError("need at least one dimension")
         for d in self.dims:
             log3_exact(d)
-        if len(set(self.dims)) > 1:
-            # Sec. 5 only treats square tori; rectangular shapes need a rotation rule the paper
-            # does not give.
-            raise ValueError("unequal torus dimensions are not covered by the paper's rotation")
 
     @property
     def D(self) -> int:
@@ -93,9 +94,23 @@ def step_dim_and_distance(torus: Torus, c: int, t: int) -> tuple:
     """(dimension, distance) used by collective c at global step t.
 
     Ring: distance 3^t (Sec. 4.1). Torus: the collectives rotate through the dimensions
-    (Sec. 5), with per-dimension step k = t div D (Appendix B, t = d + D k)."""
+    (Sec. 5), with per-dimension step k = t div D (Appendix B, t = d + D k). Unequal sides: see
+    the module docstring."""
+    return _rotation(torus, c)[t]
+
+
+@lru_cache(maxsize=None)
+def _rotation(torus: Torus, c: int) -> tuple:
     D = torus.D
-    return (c + t) % D, 3 ** (t // D)
+    left = [log3_exact(d) for d in torus.dims]
+    taken = [0] * D
+    out = []
+    for t in range(torus.steps):
+        order = [(c + t + i) % D for i in range(D)]
+        dim = next(d for d in order if taken[d] < left[d])
+        out.append((dim, 3 ** taken[dim]))
+        taken[dim] += 1
+    return tuple(out)
 
 
 def peers(torus: Torus, c: int, r: int, t: int) -> tuple:

@@ -7,7 +7,8 @@
 // Trivance (Sec. 4.1), +3^k and +2*3^k for the Bruck comparison pattern (Sec. 2.4, Fig. 1).
 //
 // One 64-thread workgroup handles one (pass, dimension, line) triple, a line being the ring of
-// ranks that differ only in that dimension's coordinate. Each message adds +1 over a cyclic range
+// ranks that differ only in that dimension's coordinate (dimensions with longer sides have fewer
+// lines; their surplus workgroups exit at once). Each message adds +1 over a cyclic range
 // of directed links; the workgroup records the range ends in an LDS difference array (plus a
 // count of ranges that wrap past position 0) and turns it into per-link loads with a wavefront
 // inclusive scan. Every output entry is written, so no clearing pass is needed.
@@ -20,7 +21,7 @@
 namespace trivance {
 namespace {
 
-constexpr int kMaxPasses = 48;
+constexpr int kMaxPasses = 40;
 constexpr int kMaxSide = 6561;  // LDS: two difference arrays of side + 1 ints
 
 struct CongArgs {
@@ -29,10 +30,10 @@ struct CongArgs {
     int npasses;
     int bruck;
     int shortest;
-    int lines;  // lines per dimension: n / side
+    int max_lines;  // lines of the dimension with the smallest side: n / min side
     int dims[kMaxDims];
     int strides[kMaxDims];
-    int distance[kMaxPasses];
+    int distance[kMaxPasses][kMaxDims];  // per pass and collective
     int act_dim[kMaxPasses][kMaxDims];
 };
 
@@ -79,13 +80,14 @@ __global__ __launch_bounds__(64) void congestion_kernel(int64_t* __restrict__ lo
     extern __shared__ int lds[];
     const int lane = threadIdx.x;
     const uint32_t wg = blockIdx.x;
-    const int line = (int)(wg % (uint32_t)a.lines);
-    const uint32_t rest = wg / (uint32_t)a.lines;
+    const int line = (int)(wg % (uint32_t)a.max_lines);
+    const uint32_t rest = wg / (uint32_t)a.max_lines;
     const int dim = (int)(rest % (uint32_t)a.D);
     const int pass = (int)(rest / (uint32_t)a.D);
 
     const int side = a.dims[dim];
     const int stride = a.strides[dim];
+    if (line >= a.n / side) return;  // this dimension has fewer lines (unequal sides)
     const int line_base = (line % stride) + (line / stride) * stride * side;
     int* plus = lds;               // side + 1 entries
     int* minus = lds + side + 1;   // side + 1 entries
@@ -94,10 +96,10 @@ __global__ __launch_bounds__(64) void congestion_kernel(int64_t* __restrict__ lo
     for (int x = lane; x < 2 * side + 4; x += 64) lds[x] = 0;
     __syncthreads();
 
-    const int dist = a.distance[pass];
     for (int x = lane; x < side; x += 64) {
         for (int c = 0; c < a.D; ++c) {
             if (a.act_dim[pass][c] != dim) continue;
+            const int dist = a.distance[pass][c];
             const int off0 = a.bruck ? dist : -dist;
             const int off1 = a.bruck ? 2 * dist : dist;
             for (int m = 0; m < 2; ++m) {
@@ -164,8 +166,8 @@ int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topol
     if (need == 0) return TRIVANCE_OK;
     if (!loads_dev) return TRIVANCE_EINVAL;
     if (P > trivance::kMaxPasses) return TRIVANCE_EUNSUPPORTED;
-    const int side = plan->dims[0];
-    if (side > trivance::kMaxSide) return TRIVANCE_EUNSUPPORTED;
+    for (int d = 0; d < plan->D; ++d)
+        if (plan->dims[d] > trivance::kMaxSide) return TRIVANCE_EUNSUPPORTED;
 
     CongArgs a{};
     a.n = plan->n;
@@ -173,17 +175,23 @@ int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topol
     a.npasses = P;
     a.bruck = plan->variant == TRIVANCE_BRUCK_REF ? 1 : 0;
     a.shortest = routing == TRIVANCE_ROUTE_SHORTEST ? 1 : 0;
-    a.lines = plan->n / side;
+    int min_side = plan->dims[0];
+    for (int d = 1; d < plan->D; ++d) min_side = plan->dims[d] < min_side ? plan->dims[d] : min_side;
+    a.max_lines = plan->n / min_side;
     for (int d = 0; d < trivance::kMaxDims; ++d) {
         a.dims[d] = d < plan->D ? plan->dims[d] : 1;
         a.strides[d] = d < plan->D ? plan->strides[d] : 1;
     }
+    int max_side = 1;
+    for (int d = 0; d < plan->D; ++d) max_side = plan->dims[d] > max_side ? plan->dims[d] : max_side;
     for (int p = 0; p < P; ++p) {
-        a.distance[p] = plan->passes[p].distance;
-        for (int c = 0; c < trivance::kMaxDims; ++c) a.act_dim[p][c] = plan->passes[p].dim[c];
+        for (int c = 0; c < trivance::kMaxDims; ++c) {
+            a.act_dim[p][c] = plan->passes[p].dim[c];
+            a.distance[p][c] = plan->passes[p].distance[c];
+        }
     }
-    const uint32_t grid = (uint32_t)((int64_t)P * plan->D * a.lines);
-    const size_t lds = (size_t)(2 * side + 4) * sizeof(int);
+    const uint32_t grid = (uint32_t)((int64_t)P * plan->D * a.max_lines);
+    const size_t lds = (size_t)(2 * max_side + 4) * sizeof(int);
     hipLaunchKernelGGL(trivance::congestion_kernel, dim3(grid), dim3(64), lds,
                        reinterpret_cast<hipStream_t>(stream), loads_dev, a);
     return hipGetLastError() == hipSuccess ? TRIVANCE_OK : TRIVANCE_EHIP;

@@ -69,8 +69,10 @@ struct StepArgs {
     int strides[kMaxDims];
     int act_dim[kMaxDims];         // active dimension per collective
     int modulus[kMaxDims][kMaxDims];
-    int distance;
-    // latency step
+    int dist[kMaxDims];            // peer distance per collective
+    // latency step (one launch covers collectives c_first .. c_first + ncoll - 1, which share
+    // the cycle length)
+    int c_first;
     int ncycles;                   // cycles per collective
     int colblocks;                 // thread blocks per (collective, cycle)
     // block steps
@@ -166,12 +168,12 @@ __global__ __launch_bounds__(kBlockThreads) void latency_step_kernel(T* __restri
     const uint32_t cb = wg % (uint32_t)a.colblocks;
     const uint32_t rest = wg / (uint32_t)a.colblocks;
     const int cyc = (int)(rest % (uint32_t)a.ncycles);
-    const int c = (int)(rest / (uint32_t)a.ncycles);
+    const int c = a.c_first + (int)(rest / (uint32_t)a.ncycles);
 
     const int dim = a.act_dim[c];
     const int side = a.dims[dim];
     const int stride = a.strides[dim];
-    const int dist = a.distance;
+    const int dist = a.dist[c];
     const int len = side / dist;  // cycle length, a power of three >= 3
     const int res = cyc % dist;
     const int other = cyc / dist;
@@ -258,14 +260,14 @@ __global__ __launch_bounds__(64 * P) void latency_split_kernel(T* __restrict__ b
     const uint32_t cb = wg % (uint32_t)a.colblocks;
     const uint32_t rest = wg / (uint32_t)a.colblocks;
     const int cyc = (int)(rest % (uint32_t)a.ncycles);
-    const int c = (int)(rest / (uint32_t)a.ncycles);
+    const int c = a.c_first + (int)(rest / (uint32_t)a.ncycles);
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
 
     const int dim = a.act_dim[c];
     const int side = a.dims[dim];
     const int stride = a.strides[dim];
-    const int dist = a.distance;
+    const int dist = a.dist[c];
     const int res = cyc % dist;
     const int other = cyc / dist;
     const int first_rank = (other % stride) + (other / stride) * stride * side + res * stride;
@@ -344,7 +346,7 @@ __device__ __forceinline__ bool decode_unit(const StepArgs& a, uint32_t unit, in
     }
     const int side = a.dims[act];
     const int st = a.strides[act];
-    const int dist = a.distance;
+    const int dist = a.dist[c];
     out->rank = (int)r;
     out->left = (int)r_act >= dist ? (int)r - dist * st : (int)r + (side - dist) * st;
     out->right = (int)r_act + dist < side ? (int)r + dist * st : (int)r - (side - dist) * st;
@@ -427,6 +429,7 @@ struct Launch {
     uint32_t grid = 0;
     int U = 0;            // block steps: 16-byte vectors per lane per chunk
     int64_t max_vec = 0;  // latency steps: column vectors of the longest segment
+    int ncoll = 0;        // latency steps: collectives in this launch group
 };
 
 // Arguments common to every pass of one call.
@@ -456,9 +459,9 @@ inline int base_args(const trivance_plan_t* p, int64_t elems, StepArgs* out, int
 template <int VEC>
 inline int pass_args(const trivance_plan_t* p, const Pass& ps, int64_t max_blk, int chunk_vecs,
                      StepArgs* a, Launch* L) {
-    a->distance = ps.distance;
     for (int c = 0; c < kMaxDims; ++c) {
         a->act_dim[c] = ps.dim[c];
+        a->dist[c] = ps.distance[c];
         for (int d = 0; d < kMaxDims; ++d) {
             const int m = c < p->D && d < p->D ? ps.modulus[c][d] : 1;
             a->modulus[c][d] = m;
@@ -466,8 +469,6 @@ inline int pass_args(const trivance_plan_t* p, const Pass& ps, int64_t max_blk, 
             a->f_nq[c][d] = make_fastdiv((uint32_t)(a->dims[d] / m));
         }
     }
-    const int side = p->dims[ps.dim[0]];
-    a->ncycles = (p->n / side) * ps.distance;
     a->kept = (int)ps.kept_per_rank;
     if (ps.phase == TRIVANCE_PHASE_LATENCY) {
         int64_t max_seg = 0;
@@ -477,12 +478,9 @@ inline int pass_args(const trivance_plan_t* p, const Pass& ps, int64_t max_blk, 
             max_seg = std::max(max_seg, e - b);
         }
         L->max_vec = (max_seg + VEC - 1) / VEC;
-        // grid for 64-column workgroups (the split-cycle kernel); the other latency kernels
-        // recompute it for 256 columns
-        a->colblocks = (int)std::max<int64_t>(1, (L->max_vec + 63) / 64);
-        const int64_t grid = (int64_t)a->D * a->ncycles * a->colblocks;
-        if (grid >= ((int64_t)1 << 31)) return TRIVANCE_EUNSUPPORTED;
-        L->grid = (uint32_t)grid;
+        // the grid is set per launch group (set_columns); check the largest one fits
+        const int64_t cols = std::max<int64_t>(1, (L->max_vec + 63) / 64);
+        if ((int64_t)a->D * p->n * cols >= ((int64_t)1 << 31)) return TRIVANCE_EUNSUPPORTED;
         return TRIVANCE_OK;
     }
     // chunk: U 16-byte vectors per lane. One (1 KiB of fp32 per row and wavefront) measured
@@ -503,10 +501,11 @@ inline int pass_args(const trivance_plan_t* p, const Pass& ps, int64_t max_blk, 
     return TRIVANCE_OK;
 }
 
-// Re-derive the grid for workgroups covering `cols` column vectors each.
+// Grid for workgroups covering `cols` column vectors each, over the a->ncoll collectives of
+// the launch group.
 inline void set_columns(StepArgs* a, Launch* L, int cols) {
     a->colblocks = (int)std::max<int64_t>(1, (L->max_vec + cols - 1) / cols);
-    L->grid = (uint32_t)((int64_t)a->D * a->ncycles * a->colblocks);
+    L->grid = (uint32_t)((int64_t)L->ncoll * a->ncycles * a->colblocks);
 }
 
 template <typename T, int VEC, int SUB, int P>
@@ -564,12 +563,26 @@ int run_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t 
         Launch L;
         rc = pass_args<VEC>(p, ps, max_blk, 1, &a, &L);
         if (rc != TRIVANCE_OK) return rc;
-        hipError_t err;
-        if (ps.phase == TRIVANCE_PHASE_LATENCY)
-            err = launch_latency<T, VEC>(buf, a, L, p->dims[ps.dim[0]] / ps.distance, stream);
-        else
+        hipError_t err = hipSuccess;
+        if (ps.phase == TRIVANCE_PHASE_LATENCY) {
+            // collectives that share a cycle length run in one launch; with equal sides that is
+            // all of them, otherwise one launch per collective
+            bool same = true;
+            for (int c = 1; c < p->D; ++c)
+                same = same && p->dims[ps.dim[c]] == p->dims[ps.dim[0]] &&
+                       ps.distance[c] == ps.distance[0];
+            for (int c0 = 0; c0 < p->D && err == hipSuccess; c0 += same ? p->D : 1) {
+                const int side = p->dims[ps.dim[c0]];
+                a.c_first = c0;
+                a.ncycles = (p->n / side) * ps.distance[c0];
+                L.ncoll = same ? p->D : 1;
+                err = launch_latency<T, VEC>(buf, a, L, side / ps.distance[c0], stream);
+            }
+            a.c_first = 0;
+        } else {
             err = launch_block<T, VEC>(buf, a, L, ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER,
                                        stream);
+        }
         if (err != hipSuccess) return TRIVANCE_EHIP;
     }
     return TRIVANCE_OK;

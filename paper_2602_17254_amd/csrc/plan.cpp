@@ -3,7 +3,10 @@
 // Steps and peers: Sec. 4.1 (pi(r, k) = r -/+ 3^k), Theorem 1 (log3 n steps), Sec. 4.2 (the
 // latency-optimal variant uses the same pattern), Sec. 5 (one collective per torus dimension on
 // 1/D of the data, switching dimension every step; Appendix B's index t = d + D k fixes the
-// per-dimension step k = t div D). Block sets: the closed form of Sec. 4.3 says that the blocks
+// per-dimension step k = t div D). Unequal sides (rectangular tori) are not covered by Sec. 5;
+// the rule used for them: collective c at global step t takes the first dimension, in cyclic
+// order from (c + t) mod D, in which it still has steps left. With equal sides this is exactly
+// (c + t) mod D at distance 3^(t div D). Block sets: the closed form of Sec. 4.3 says that the blocks
 // forwarded to peer p at step k are p + sum_{i>k} e_i 3^i; equivalently the blocks a rank keeps
 // after step k are those congruent to it modulo 3^(k+1). On a torus that congruence holds per
 // dimension, with the exponent counting the steps taken so far in that dimension.
@@ -34,21 +37,43 @@ int ipow3(int e) {
     return v;
 }
 
-// Fill the per-dimension moduli that hold after global step t for collective c.
-void fill_moduli(const trivance_plan_t* p, int t, int c, int* out) {
-    int count[kMaxDims] = {};
-    for (int s = 0; s <= t; ++s) count[(c + s) % p->D] += 1;
-    for (int d = 0; d < kMaxDims; ++d) out[d] = d < p->D ? ipow3(count[d]) : 1;
+// Per collective: the dimension and distance of every global step, and the per-dimension
+// moduli 3^(steps taken so far in that dimension) after every step.
+struct Rotation {
+    int dim[64][kMaxDims];
+    int dist[64][kMaxDims];
+    int modulus[64][kMaxDims][kMaxDims];
+};
+
+void fill_rotation(const trivance_plan_t* p, const int* steps_per_dim, Rotation* rot) {
+    for (int c = 0; c < p->D; ++c) {
+        int count[kMaxDims] = {};
+        for (int t = 0; t < p->S; ++t) {
+            int d = (c + t) % p->D;
+            for (int i = 0; i < p->D; ++i) {
+                const int cand = (c + t + i) % p->D;
+                if (count[cand] < steps_per_dim[cand]) {
+                    d = cand;
+                    break;
+                }
+            }
+            rot->dim[t][c] = d;
+            rot->dist[t][c] = ipow3(count[d]);
+            count[d] += 1;
+            for (int dd = 0; dd < kMaxDims; ++dd)
+                rot->modulus[t][c][dd] = dd < p->D ? ipow3(count[dd]) : 1;
+        }
+    }
 }
 
-Pass make_pass(const trivance_plan_t* p, int phase, int t) {
+Pass make_pass(const trivance_plan_t* p, const Rotation& rot, int phase, int t) {
     Pass ps{};
     ps.phase = phase;
     ps.step = t;
-    ps.distance = ipow3(t / p->D);
     for (int c = 0; c < kMaxDims; ++c) {
-        ps.dim[c] = c < p->D ? (c + t) % p->D : 0;
-        if (c < p->D) fill_moduli(p, t, c, ps.modulus[c]);
+        ps.dim[c] = c < p->D ? rot.dim[t][c] : 0;
+        ps.distance[c] = c < p->D ? rot.dist[t][c] : 1;
+        for (int d = 0; d < kMaxDims; ++d) ps.modulus[c][d] = c < p->D ? rot.modulus[t][c][d] : 1;
     }
     ps.kept_per_rank = p->n / ipow3(t + 1);
     return ps;
@@ -109,10 +134,8 @@ int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance
         }
         if (prod != n) return TRIVANCE_EINVAL;
     }
-    for (int d = 0; d < D; ++d) {
+    for (int d = 0; d < D; ++d)
         if (log3_exact(dims[d]) < 0) return TRIVANCE_EUNSUPPORTED;
-        if (dims[d] != dims[0]) return TRIVANCE_EUNSUPPORTED;
-    }
     if (variant == TRIVANCE_BRUCK_REF && D != 1) return TRIVANCE_EUNSUPPORTED;
 
     trivance_plan_t* p = new (std::nothrow) trivance_plan_t;
@@ -121,26 +144,40 @@ int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance
     p->D = D;
     p->variant = variant;
     int stride = 1;
+    int steps_per_dim[kMaxDims] = {};
     for (int d = 0; d < D; ++d) {
         p->dims[d] = dims[d];
         p->strides[d] = stride;
         stride *= dims[d];
-        p->S += log3_exact(dims[d]);
+        steps_per_dim[d] = log3_exact(dims[d]);
+        p->S += steps_per_dim[d];
     }
-    try {
-        if (variant == TRIVANCE_BANDWIDTH_OPT) {
-            for (int t = 0; t < p->S; ++t)
-                p->passes.push_back(make_pass(p, TRIVANCE_PHASE_REDUCE_SCATTER, t));
-            for (int t = p->S - 1; t >= 0; --t)
-                p->passes.push_back(make_pass(p, TRIVANCE_PHASE_ALLGATHER, t));
-        } else {
-            for (int t = 0; t < p->S; ++t)
-                p->passes.push_back(make_pass(p, TRIVANCE_PHASE_LATENCY, t));
-        }
-    } catch (const std::bad_alloc&) {
+    if (p->S > 64) {
+        delete p;
+        return TRIVANCE_EUNSUPPORTED;
+    }
+    Rotation* rot = new (std::nothrow) Rotation;
+    if (!rot) {
         delete p;
         return TRIVANCE_ENOMEM;
     }
+    fill_rotation(p, steps_per_dim, rot);
+    try {
+        if (variant == TRIVANCE_BANDWIDTH_OPT) {
+            for (int t = 0; t < p->S; ++t)
+                p->passes.push_back(make_pass(p, *rot, TRIVANCE_PHASE_REDUCE_SCATTER, t));
+            for (int t = p->S - 1; t >= 0; --t)
+                p->passes.push_back(make_pass(p, *rot, TRIVANCE_PHASE_ALLGATHER, t));
+        } else {
+            for (int t = 0; t < p->S; ++t)
+                p->passes.push_back(make_pass(p, *rot, TRIVANCE_PHASE_LATENCY, t));
+        }
+    } catch (const std::bad_alloc&) {
+        delete rot;
+        delete p;
+        return TRIVANCE_ENOMEM;
+    }
+    delete rot;
     *out = p;
     return TRIVANCE_OK;
 }
@@ -164,7 +201,7 @@ int trivance_plan_step(const trivance_plan_t* plan, int pass, int collective, in
     if (phase) *phase = ps.phase;
     if (step) *step = ps.step;
     if (dim) *dim = ps.dim[collective];
-    if (distance) *distance = ps.distance;
+    if (distance) *distance = ps.distance[collective];
     return TRIVANCE_OK;
 }
 

@@ -14,9 +14,9 @@ constexpr int kGranule = 64;  // elements per partition granule (256 B of fp32 /
 // One kernel-materialised step.
 struct Pass {
     int phase;           // trivance_phase
-    int step;            // global step index t
-    int distance;        // 3^(t div D)
-    int dim[kMaxDims];   // active dimension of each collective
+    int step;                 // global step index t
+    int distance[kMaxDims];   // peer distance of each collective: 3^(steps it took before in dim)
+    int dim[kMaxDims];        // active dimension of each collective
     // modulus[c][d] = 3^(number of steps <= t that collective c has taken in dimension d).
     // Rank r keeps block j after reduce-scatter step t iff j_d == r_d (mod modulus[c][d]) for
     // every d; the same pairs (r, j) are the senders of all-gather step t.

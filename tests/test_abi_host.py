@@ -36,7 +36,8 @@ def test_exports_every_declared_symbol():
 
 @pytest.mark.parametrize("dims,variant", [((1,), "L"), ((3,), "B"), ((9,), "L"), ((81,), "L"),
                                           ((243,), "B"), ((27, 27), "B"), ((9, 9, 9), "B"),
-                                          ((27, 27), "L"), ((9, 9, 9), "L"), ((81,), "BRUCK")])
+                                          ((27, 27), "L"), ((9, 9, 9), "L"), ((81,), "BRUCK"),
+                                          ((9, 27), "B"), ((27, 3), "L"), ((3, 9, 27), "B")])
 def test_plan_matches_oracle_schedule(dims, variant):
     p = T.trivance_plan(dims, variant)
     t = schedule.Torus(dims)
@@ -86,7 +87,7 @@ def test_plan_errors():
         T.trivance_plan((8,), "L")
     assert e.value.status == -2
     with pytest.raises(T.TrivanceError) as e:
-        T.trivance_plan((9, 27), "B")
+        T.trivance_plan((9, 8), "B")
     assert e.value.status == -2
     with pytest.raises(T.TrivanceError) as e:
         T.trivance_plan((9, 9), "BRUCK")

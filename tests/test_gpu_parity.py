@@ -45,6 +45,9 @@ SHAPES = [
     ((3, 3, 3), 64 * 27 * 3 + 16), ((3, 3, 3), 999),
     ((27, 27), 64 * 729 + 36),
     ((9, 9, 9), 64 * 729 * 2 + 100),
+    # rectangular tori (unequal sides; rotation reading in include/trivance.h)
+    ((3, 9), 64 * 27 * 3 + 4), ((9, 3), 777), ((3, 27), 64 * 81 * 2 + 12),
+    ((27, 3), 64 * 81 + 8), ((3, 3, 9), 64 * 81 * 2 + 4), ((9, 27), 64 * 243 + 4),
 ]
 
 
@@ -90,7 +93,7 @@ def test_misaligned_rows_use_scalar_path():
         assert_matches_oracle(view.cpu().numpy(), V, dims, variant, what="misaligned")
 
 
-@pytest.mark.parametrize("dims", [(27,), (9, 9), (3, 3, 3)])
+@pytest.mark.parametrize("dims", [(27,), (9, 9), (3, 3, 3), (3, 9)])
 def test_step_hook_coverage(dims):
     """Lemma 2 on the GPU: with one-hot int32 inputs, after each latency-optimal pass every rank
     holds each source of its covered window exactly once; passes run one call at a time equal the
@@ -148,6 +151,7 @@ def test_step_hook_reduce_scatter_then_resume(dims):
     ((27, 27), "B", "scheduled"), ((9, 9, 9), "B", "scheduled"), ((27, 27), "L", "shortest"),
     ((9,), "BRUCK", "scheduled"), ((81,), "BRUCK", "scheduled"), ((9,), "BRUCK", "shortest"),
     ((243,), "BRUCK", "shortest"), ((3, 3), "B", "shortest"), ((1,), "L", "scheduled"),
+    ((9, 27), "B", "scheduled"), ((3, 9), "L", "shortest"), ((3, 3, 9), "B", "scheduled"),
 ])
 def test_congestion_bit_exact(dims, variant, routing):
     import paper_2602_17254_amd as T

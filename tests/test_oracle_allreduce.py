@@ -18,7 +18,7 @@ import pytest
 
 from oracle import allreduce, partition, schedule
 
-TOPOS = [(1,), (3,), (9,), (27,), (81,), (3, 3), (9, 9), (3, 3, 3)]
+TOPOS = [(1,), (3,), (9,), (27,), (81,), (3, 3), (9, 9), (3, 3, 3), (3, 9), (27, 3), (3, 9, 3)]
 ELEMS = [0, 1, 3, 63, 64, 65, 200, 1023]
 
 
@@ -106,7 +106,7 @@ def test_association_is_observable():
     assert np.float32(1.0) + (e + e) != np.float32(1.0)
 
 
-@pytest.mark.parametrize("dims", [(9,), (27,), (81,), (9, 9), (3, 3, 3)])
+@pytest.mark.parametrize("dims", [(9,), (27,), (81,), (9, 9), (3, 3, 3), (3, 27), (9, 3, 3)])
 def test_bandwidth_variant_block_equals_latency_variant_owner(dims):
     """(e): block j of the B result equals, bit for bit, rank j's L result; and B leaves every rank
     with identical bits."""

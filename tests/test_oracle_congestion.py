@@ -90,3 +90,19 @@ def test_loads_shape_and_ports():
     loads = congestion.link_loads((27, 27), "B")
     assert loads.shape == (12, 729, 4)
     assert loads.dtype == np.int64
+
+
+@pytest.mark.parametrize("dims,variant", [((3, 9), "B"), ((9, 27), "L"), ((3, 3, 9), "B")])
+def test_rectangular_link_loads(dims, variant):
+    """With unequal sides two collectives can share a dimension in a step; every directed link of
+    dimension d then carries sum over the collectives using d of 3^(their per-dimension step)."""
+    t = schedule.Torus(dims)
+    loads = congestion.link_loads(dims, variant)
+    for pi, (_, step) in enumerate(schedule.pass_list(t, variant)):
+        want = [0] * t.D
+        for c in range(t.D):
+            d, dist = schedule.step_dim_and_distance(t, c, step)
+            want[d] += dist
+        for d in range(t.D):
+            assert (loads[pi][:, 2 * d] == want[d]).all()
+            assert (loads[pi][:, 2 * d + 1] == want[d]).all()

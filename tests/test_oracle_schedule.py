@@ -32,8 +32,6 @@ def test_non_power_of_three_rejected():
     for bad in (2, 4, 8, 10, 32):
         with pytest.raises(ValueError):
             schedule.Torus((bad,))
-    with pytest.raises(ValueError):
-        schedule.Torus((9, 27))  # rectangular: no rotation rule in the paper
 
 
 def test_ring_peers_are_pm_3k():
@@ -100,7 +98,7 @@ def test_lemma2_coverage_window(n):
             np.testing.assert_array_equal(out[r], want)
 
 
-@pytest.mark.parametrize("dims", [(3, 3), (9, 9), (3, 3, 3)])
+@pytest.mark.parametrize("dims", [(3, 3), (9, 9), (3, 3, 3), (3, 9), (9, 3), (3, 3, 9)])
 def test_torus_coverage_is_product_of_ring_windows(dims):
     """Sec. 5: each collective applies the ring pattern per dimension, so after some steps the
     covered sources are the product of per-dimension Lemma-2 windows (R = (3^k - 1) / 2 after k
@@ -121,7 +119,7 @@ def test_torus_coverage_is_product_of_ring_windows(dims):
         for c in range(D):
             kd = [0] * D
             for tt in range(steps_done):
-                kd[(c + tt) % D] += 1
+                kd[schedule.step_dim_and_distance(t, c, tt)[0]] += 1
             for r in range(n):
                 rc = t.coords(r)
                 want = []
@@ -133,7 +131,8 @@ def test_torus_coverage_is_product_of_ring_windows(dims):
                 np.testing.assert_array_equal(out[r, seg_cols[c]], np.array(want, np.int32))
 
 
-@pytest.mark.parametrize("dims", [(9,), (27,), (243,), (3, 3), (9, 9), (27, 27), (9, 9, 9)])
+@pytest.mark.parametrize("dims", [(9,), (27,), (243,), (3, 3), (9, 9), (27, 27), (9, 9, 9),
+                                  (3, 27), (9, 3, 3)])
 def test_lemma1_bandwidth_and_reduction_volume(dims):
     """Lemma 1: a rank sends n - 1 blocks per reduce-scatter phase (m (1 - 1/n) bytes).
     Sec. 7 (reduction volume): the partial data reduced per rank sums to 1.5 m (1 - 1/n),
@@ -161,3 +160,20 @@ def test_dimension_rotation():
     t = schedule.Torus((9, 9))
     assert [schedule.step_dim_and_distance(t, 0, s) for s in range(4)] == [(0, 1), (1, 1), (0, 3), (1, 3)]
     assert [schedule.step_dim_and_distance(t, 1, s) for s in range(4)] == [(1, 1), (0, 1), (1, 3), (0, 3)]
+
+
+@pytest.mark.parametrize("dims", [(3, 9), (9, 27), (27, 3), (3, 3, 9), (9, 3, 27)])
+def test_rectangular_rotation_reading(dims):
+    """Unequal sides (not covered by Sec. 5): every collective takes exactly log3(side) steps in
+    each dimension, the k-th step in a dimension has distance 3^k, and while no dimension is
+    exhausted the collectives use pairwise distinct dimensions (as in Sec. 5)."""
+    t = schedule.Torus(dims)
+    for c in range(t.D):
+        seq = [schedule.step_dim_and_distance(t, c, s) for s in range(t.steps)]
+        for d in range(t.D):
+            dists = [dist for (dd, dist) in seq if dd == d]
+            assert dists == [3 ** k for k in range(schedule.log3_exact(dims[d]))]
+    short = min(schedule.log3_exact(d) for d in dims)
+    for s in range(short * t.D):
+        used = [schedule.step_dim_and_distance(t, c, s)[0] for c in range(t.D)]
+        assert len(set(used)) == t.D
