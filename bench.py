@@ -37,14 +37,14 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # source it was measured on (sha256 of the source file, first 16 hex digits).
 MEASURED_TRAFFIC = {
     # profiles/latency_split_kernel_ring81_L_8MiB.md, profiles/block_step_kernel_*.md
-    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "3ee85e63946bf549",
-                                                 "bytes_per_launch": 1359030905},
-    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "3ee85e63946bf549",
-                                                        "bytes_per_launch": 3248087063},
-    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "3ee85e63946bf549",
-                                                          "bytes_per_launch": 1017882172},
-    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "3ee85e63946bf549",
-                                                            "bytes_per_launch": 32569549948},
+    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "5caee43cd4004733",
+        "bytes_per_launch": 1359027705},
+    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "5caee43cd4004733",
+        "bytes_per_launch": 3248089764},
+    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "5caee43cd4004733",
+        "bytes_per_launch": 1017883399},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "5caee43cd4004733",
+        "bytes_per_launch": 32569577424},
 }
 
 
