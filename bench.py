@@ -37,14 +37,18 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # source it was measured on (sha256 of the source file, first 16 hex digits).
 MEASURED_TRAFFIC = {
     # profiles/latency_split_kernel_ring81_L_8MiB.md, profiles/block_step_kernel_*.md
-    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "5caee43cd4004733",
-        "bytes_per_launch": 1359027705},
-    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "5caee43cd4004733",
-        "bytes_per_launch": 3248089764},
-    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "5caee43cd4004733",
-        "bytes_per_launch": 1017883399},
-    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "5caee43cd4004733",
-        "bytes_per_launch": 32569577424},
+    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "eb1e7eb8c65a7a76",
+        "bytes_per_launch": 1359033977},
+    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
+        "bytes_per_launch": 3248087435},
+    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
+        "bytes_per_launch": 1017880551},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
+        "bytes_per_launch": 32569574523},
+    ("ring8_B_32MiB", "ring_tree_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
+        "bytes_per_launch": 251705947},
+    ("ring64_B_8MiB", "ring_tree_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
+        "bytes_per_launch": 283163090},
 }
 
 
@@ -68,15 +72,14 @@ def cpu_baseline(w, gpu_first_result_cols, cols, V_cols, seconds_target=15.0):
     if w.variant == "L":
         out = allreduce.latency_optimal(V_cols, w.dims, col_seg=seg)
     else:
-        out = allreduce.bandwidth_optimal(V_cols, w.dims, col_seg=seg, col_blk=blk)
+        out = allreduce.allreduce(V_cols, w.dims, "B", col_seg=seg, col_blk=blk)
     dt = time.perf_counter() - t0
-    S = sum(int(round(np.log(d) / np.log(3))) for d in w.dims)
-    # algorithmic bytes of the sample (same formula as the device path)
+    # algorithmic bytes of the sample: the device path's own accounting, scaled to the sample
+    import paper_2602_17254_amd as T
+
     ncols = len(cols)
-    if w.variant == "L":
-        sample_bytes = 2 * S * w.n * ncols * 4
-    else:
-        sample_bytes = int(3.5 * 4 * ncols * (w.n - 1))
+    sample_bytes = T.trivance_algorithmic_bytes(T.trivance_plan(w.dims, w.variant), w.elems) \
+        * ncols / w.elems
     same = bool(np.array_equal(out, gpu_first_result_cols))
     return {
         "value": round(sample_bytes / dt / 1e9, 4),
@@ -158,7 +161,10 @@ def run_workload(w, steps, warmup, with_cpu):
 
     # dominant kernel: the pass type with the most total time
     phases = [T.trivance_plan_step(plan, p)[0] for p in range(P)]
-    names = {0: "latency_split_kernel", 1: "block_step_kernel<reduce>", 2: "block_step_kernel<copy>"}
+    tree = len(w.dims) == 1 and 3 ** round(np.log(w.dims[0]) / np.log(3)) != w.dims[0]
+    names = {0: "latency_split_kernel",
+             1: "ring_tree_step_kernel<reduce>" if tree else "block_step_kernel<reduce>",
+             2: "ring_tree_step_kernel<copy>" if tree else "block_step_kernel<copy>"}
     tot = {}
     for p, ph in enumerate(phases):
         tot.setdefault(ph, [0.0, 0, 0])
@@ -239,7 +245,8 @@ def copy_probe(nbytes: int, reps: int = 3) -> None:
                       "GBps_read_plus_write": round(2 * nbytes / dt / 1e9, 1)}), flush=True)
 
 
-SWEEP_CLASSES = [((81,), "L"), ((243,), "B"), ((27, 27), "B"), ((9, 9, 9), "B")]
+SWEEP_CLASSES = [((81,), "L"), ((243,), "B"), ((27, 27), "B"), ((9, 9, 9), "B"), ((8,), "B"),
+                 ((64,), "B")]
 SWEEP_MIB = [8, 16, 32, 64, 128]
 
 

@@ -24,7 +24,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import partition, schedule
+from . import nonpow3, partition, schedule
 
 
 def _check_input(V: np.ndarray, torus: schedule.Torus) -> None:
@@ -175,6 +175,10 @@ def bandwidth_optimal(V: np.ndarray, dims, col_seg=None, col_blk=None, rs_passes
 
 
 def allreduce(V: np.ndarray, dims, variant: str, **kw) -> np.ndarray:
+    if len(dims) == 1 and dims[0] >= 2 and nonpow3.levels(dims[0])[1] != 0:
+        if variant != "B":
+            raise ValueError("rings whose size is not a power of three: bandwidth-optimal only")
+        return nonpow3.bandwidth_optimal_ring(V, col_blk=kw.get("col_blk"))
     if variant == "L":
         return latency_optimal(V, dims, **kw)
     if variant == "B":

@@ -30,7 +30,7 @@ from fractions import Fraction
 
 import numpy as np
 
-from . import schedule
+from . import nonpow3, schedule
 
 
 def _messages(torus: schedule.Torus, variant: str, c: int, r: int, t: int):
@@ -69,6 +69,8 @@ def passes_of(torus: schedule.Torus, variant: str) -> list:
 
 
 def link_loads(dims, variant: str, routing: str = "scheduled") -> np.ndarray:
+    if len(dims) == 1 and variant == "B" and dims[0] >= 2 and nonpow3.levels(dims[0])[1] != 0:
+        return nonpow3.link_loads_ring(dims[0])  # Sec. 4.4 ring; distances < n/2 either way
     torus = schedule.Torus(tuple(dims))
     plist = passes_of(torus, variant)
     n, D = torus.n, torus.D

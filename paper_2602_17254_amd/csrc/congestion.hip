@@ -34,6 +34,7 @@ struct CongArgs {
     int dims[kMaxDims];
     int strides[kMaxDims];
     int distance[kMaxPasses][kMaxDims];  // per pass and collective
+    int dirs[kMaxPasses];                // Trivance passes: bit 0 messages towards +, bit 1 towards -
     int act_dim[kMaxPasses][kMaxDims];
 };
 
@@ -103,6 +104,7 @@ __global__ __launch_bounds__(64) void congestion_kernel(int64_t* __restrict__ lo
             const int off0 = a.bruck ? dist : -dist;
             const int off1 = a.bruck ? 2 * dist : dist;
             for (int m = 0; m < 2; ++m) {
+                if (!a.bruck && !(a.dirs[pass] & (m == 0 ? 2 : 1))) continue;
                 int dir, hops;
                 route(m == 0 ? off0 : off1, side, a.shortest != 0, &dir, &hops);
                 if (hops == 0) continue;
@@ -188,6 +190,14 @@ int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topol
         for (int c = 0; c < trivance::kMaxDims; ++c) {
             a.act_dim[p][c] = plan->passes[p].dim[c];
             a.distance[p][c] = plan->passes[p].distance[c];
+        }
+        a.dirs[p] = 3;
+        if (plan->tree) {
+            // a reduce-scatter step sends child -> parent; its all-gather step retraces the
+            // messages, so the directions swap
+            const int m = plan->tree_dirs[plan->passes[p].step];
+            a.dirs[p] = plan->passes[p].phase == TRIVANCE_PHASE_REDUCE_SCATTER
+                            ? m : (((m & 1) << 1) | ((m & 2) >> 1));
         }
     }
     const uint32_t grid = (uint32_t)((int64_t)P * plan->D * a.max_lines);

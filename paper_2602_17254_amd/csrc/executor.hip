@@ -422,6 +422,80 @@ __global__ __launch_bounds__(kBlockThreads) void block_step_kernel(T* __restrict
 }
 
 // ---------------------------------------------------------------------------------------------
+// Ring of any size (Sec. 4.4): every block is reduced along one tree (see plan.cpp). A step lists
+// its receivers as offsets from the block's owner with the sides their children send from; the
+// reduce-scatter computes x <- (x + from_left) + from_right with absent terms skipped, the
+// all-gather copies x to the children. Each rank forwards each block once, so within a step no
+// location is both read by a neighbour and written: the update is in place.
+struct TreeArgs {
+    int64_t elems;
+    int64_t G;            // granules per rank vector
+    int n;
+    int dist;
+    int narrow;           // 1 if n * (G + 1) < 2^31
+    int cpb;              // chunks per block
+    int nrecv;
+    uint32_t total_units;  // n * nrecv * cpb
+    FastDiv f_cpb, f_nrecv, f_n;
+    uint32_t recv[kMaxRecv];
+};
+
+template <typename T, int VEC, bool REDUCE>
+__global__ __launch_bounds__(kBlockThreads) void ring_tree_step_kernel(T* __restrict__ buf,
+                                                                        TreeArgs a) {
+    using V = Vec<T, VEC>;
+    constexpr int kChunk = 64 * VEC;
+    const int lane = threadIdx.x & 63;
+    const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t wg = xcd_contiguous(blockIdx.x, gridDim.x);
+    const uint32_t unit = wg * (uint32_t)kWavesPerBlock + wave;
+    if (unit >= a.total_units) return;
+    const uint32_t pair = fdiv(unit, a.f_cpb);
+    const uint32_t chunk = unit - pair * (uint32_t)a.cpb;
+    const uint32_t j = fdiv(pair, a.f_nrecv);
+    const uint32_t i = pair - j * (uint32_t)a.nrecv;
+    const uint32_t entry = a.recv[i];
+    const uint32_t off = entry & 0x3FFFFFFFu;
+    uint32_t x = j + off;
+    if (x >= (uint32_t)a.n) x -= a.n;
+    const uint32_t left = x >= (uint32_t)a.dist ? x - a.dist : x + a.n - a.dist;
+    uint32_t right = x + a.dist;
+    if (right >= (uint32_t)a.n) right -= a.n;
+
+    int64_t gb, ge;
+    if (a.narrow) {
+        gb = fdiv(j * (uint32_t)a.G, a.f_n);
+        ge = fdiv((j + 1) * (uint32_t)a.G, a.f_n);
+    } else {
+        gb = (int64_t)j * a.G / a.n;
+        ge = (int64_t)(j + 1) * a.G / a.n;
+    }
+    const int64_t E = a.elems;
+    const int64_t b = imin64(gb * kGranule, E);
+    const int64_t e = imin64(ge * kGranule, E);
+    const int64_t idx = b + (int64_t)chunk * kChunk + (int64_t)lane * VEC;
+    if (idx >= e) return;
+    T* const own = buf + (int64_t)x * E + idx;
+    T* const pl = buf + (int64_t)left * E + idx;
+    T* const pr = buf + (int64_t)right * E + idx;
+    const bool from_left = (entry & kFromLeft) != 0;
+    const bool from_right = (entry & kFromRight) != 0;
+    if constexpr (REDUCE) {
+        V acc = ld<T, VEC, true>(own);
+        V l, r;
+        if (from_left) l = ld<T, VEC, true>(pl);
+        if (from_right) r = ld<T, VEC, true>(pr);
+        if (from_left) acc = vadd(acc, l);
+        if (from_right) acc = vadd(acc, r);
+        st<T, VEC, true>(own, acc);
+    } else {
+        const V v = ld<T, VEC, true>(own);
+        if (from_left) st<T, VEC, true>(pl, v);
+        if (from_right) st<T, VEC, true>(pr, v);
+    }
+}
+
+// ---------------------------------------------------------------------------------------------
 // Host side.
 
 // Launch geometry of one pass.
@@ -588,9 +662,49 @@ int run_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t 
     return TRIVANCE_OK;
 }
 
+template <typename T, int VEC>
+int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
+                    int pe) {
+    TreeArgs a;
+    a.elems = elems;
+    a.G = (elems + kGranule - 1) / kGranule;
+    a.n = p->n;
+    a.narrow = (int64_t)p->n * (a.G + 1) < ((int64_t)1 << 31) ? 1 : 0;
+    a.f_n = make_fastdiv((uint32_t)p->n);
+    const int64_t max_blk = max_block_granules(p, elems) * kGranule;
+    a.cpb = (int)std::max<int64_t>(1, (max_blk + 64 * VEC - 1) / (64 * VEC));
+    a.f_cpb = make_fastdiv((uint32_t)a.cpb);
+    for (int pi = pb; pi < pe; ++pi) {
+        const Pass& ps = p->passes[pi];
+        const std::vector<uint32_t>& recv = p->tree_recv[ps.step];
+        a.dist = p->tree_dist[ps.step];
+        a.nrecv = (int)recv.size();
+        if (a.nrecv == 0) continue;
+        for (int i = 0; i < a.nrecv; ++i) a.recv[i] = recv[i];
+        a.f_nrecv = make_fastdiv((uint32_t)a.nrecv);
+        const int64_t total = (int64_t)p->n * a.nrecv * a.cpb;
+        if (total >= ((int64_t)1 << 31) - kWavesPerBlock) return TRIVANCE_EUNSUPPORTED;
+        a.total_units = (uint32_t)total;
+        const dim3 grid((uint32_t)((total + kWavesPerBlock - 1) / kWavesPerBlock));
+        if (ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER)
+            hipLaunchKernelGGL((ring_tree_step_kernel<T, VEC, true>), grid, dim3(kBlockThreads),
+                               0, stream, buf, a);
+        else
+            hipLaunchKernelGGL((ring_tree_step_kernel<T, VEC, false>), grid,
+                               dim3(kBlockThreads), 0, stream, buf, a);
+        if (hipGetLastError() != hipSuccess) return TRIVANCE_EHIP;
+    }
+    return TRIVANCE_OK;
+}
+
 template <typename T>
 int run_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
                int pe) {
+    if (p->tree) {
+        if (elems % 4 == 0 && (uintptr_t)buf % 16 == 0)
+            return run_tree_passes<T, 4>(buf, elems, p, stream, pb, pe);
+        return run_tree_passes<T, 1>(buf, elems, p, stream, pb, pe);
+    }
     // 16-byte vectors need 16-byte aligned rows: an aligned base and elems % 4 == 0
     if (elems % 4 == 0 && (uintptr_t)buf % 16 == 0)
         return run_passes_vec<T, 4>(buf, elems, p, stream, pb, pe);

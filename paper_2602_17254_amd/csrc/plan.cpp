@@ -10,6 +10,7 @@
 // forwarded to peer p at step k are p + sum_{i>k} e_i 3^i; equivalently the blocks a rank keeps
 // after step k are those congruent to it modulo 3^(k+1). On a torus that congruence holds per
 // dimension, with the exponent counting the steps taken so far in that dimension.
+#include <cmath>
 #include <cstdlib>
 #include <new>
 
@@ -79,6 +80,136 @@ Pass make_pass(const trivance_plan_t* p, const Rotation& rot, int phase, int t) 
     return ps;
 }
 
+// ---- rings whose size is not a power of three (Sec. 4.4) ----
+//
+// f full steps at distances 3^0..3^(f-1), then a final step at d = ceil((n - 3^f) / 2). Every
+// block j is reduced along one tree so that each rank forwards each block once (Sec. 4.4); the
+// tree is read from three ordinary Trivance trees rooted at offsets 0, +d and -d from j (offsets
+// in (-n/2, n/2]): ranks beyond j's window (|offset| > R = (3^f - 1)/2) start in the tree of
+// their side; then, until nothing changes, every rank on the path of a +/- member joins that
+// tree, and a member of j's tree whose path meets another tree joins it. The root offsets +d
+// and -d hand their partials to j in the final step.
+
+// Balanced-ternary digits of v (lowest first, f of them); false if v needs more digits.
+bool balanced_digits(long v, int f, int* e) {
+    for (int i = 0; i < f; ++i) {
+        const int r = (int)(((v % 3) + 3) % 3);
+        e[i] = r == 2 ? -1 : r;
+        v = (v - e[i]) / 3;
+    }
+    return v == 0;
+}
+
+int build_tree(trivance_plan_t* p) {
+    const int n = p->n;
+    int f = 0;
+    long pw = 1;
+    while (pw * 3 <= n) {
+        pw *= 3;
+        ++f;
+    }
+    const long R = (pw - 1) / 2;
+    const long d = (n - pw + 1) / 2;
+    const long lo = -((n - 1) / 2);
+    auto canon = [&](long o) {
+        long r = (o - lo) % n;
+        if (r < 0) r += n;
+        return r + lo;
+    };
+    auto idx = [&](long o) { return (size_t)(canon(o) - lo); };
+    std::vector<int> fam(n);
+    for (long o = lo; o < lo + n; ++o) fam[idx(o)] = o > R ? 1 : (o < -R ? -1 : 0);
+    // offset of rank o relative to the root of tree `side`, if o lies in that tree's window
+    auto rel_in = [&](long o, int side, long* rel) {
+        const long cands[3] = {o, o + n, o - n};
+        for (long c : cands) {
+            const long r = c - side * d;
+            if (r >= -R && r <= R) {
+                *rel = r;
+                return true;
+            }
+        }
+        return false;
+    };
+    int e[32];
+    for (int guard = 0;; ++guard) {
+        if (guard > 4 * n + 8) return TRIVANCE_EUNSUPPORTED;
+        bool changed = false;
+        for (long o = lo; o < lo + n; ++o) {
+            const int side = fam[idx(o)];
+            long rel;
+            if (!rel_in(o, side, &rel) || !balanced_digits(rel, f, e)) return TRIVANCE_EUNSUPPORTED;
+            long pos = rel;
+            long pw_i = 1;
+            for (int i = 0; i < f; ++i, pw_i *= 3) {
+                pos -= e[i] * pw_i;
+                const long q = canon(pos + side * d);
+                if (side != 0 && fam[idx(q)] != side) {
+                    if (fam[idx(q)] != 0 || q == 0) return TRIVANCE_EUNSUPPORTED;
+                    fam[idx(q)] = side;
+                    changed = true;
+                }
+                if (side == 0 && fam[idx(q)] != 0) {
+                    fam[idx(o)] = fam[idx(q)];
+                    changed = true;
+                    break;
+                }
+            }
+        }
+        if (!changed) break;
+    }
+    if (fam[idx(0)] != 0) return TRIVANCE_EUNSUPPORTED;
+
+    // send step, direction and parent of every offset; receivers per step
+    const int S = f + 1;
+    std::vector<int> step(n, S), dir(n, 0);
+    std::vector<long> parent(n, 0);
+    for (long o = lo; o < lo + n; ++o) {
+        if (o == 0) continue;
+        const int side = fam[idx(o)];
+        long rel;
+        rel_in(o, side, &rel);
+        balanced_digits(rel, f, e);
+        int k = f;
+        int ek = side;
+        long pw_k = 1;
+        for (int i = 0; i < f; ++i, pw_k *= 3) {
+            if (e[i] != 0) {
+                k = i;
+                ek = e[i];
+                break;
+            }
+        }
+        const long dist = k < f ? pw_k : d;
+        step[idx(o)] = k;
+        dir[idx(o)] = ek;
+        parent[idx(o)] = canon(o - ek * dist);
+    }
+    p->tree_dist.assign(S, 0);
+    p->tree_dirs.assign(S, 0);
+    p->tree_recv.assign(S, std::vector<uint32_t>());
+    for (int k = 0; k < S; ++k) p->tree_dist[k] = k < f ? ipow3(k) : (int)d;
+    std::vector<std::vector<uint32_t>> flags(S, std::vector<uint32_t>(n, 0));
+    for (long o = lo; o < lo + n; ++o) {
+        if (o == 0) continue;
+        const int k = step[idx(o)];
+        const long par = parent[idx(o)];
+        if (par != 0 && step[idx(par)] <= k) return TRIVANCE_EUNSUPPORTED;  // not a tree
+        flags[k][idx(par)] |= dir[idx(o)] > 0 ? trivance::kFromRight : trivance::kFromLeft;
+        p->tree_dirs[k] |= dir[idx(o)] > 0 ? 2 : 1;
+    }
+    for (int k = 0; k < S; ++k) {
+        for (long o = lo; o < lo + n; ++o) {
+            const uint32_t fl = flags[k][idx(o)];
+            if (fl) p->tree_recv[k].push_back((uint32_t)((o % n + n) % n) | fl);
+        }
+        if ((int)p->tree_recv[k].size() > trivance::kMaxRecv) return TRIVANCE_EUNSUPPORTED;
+    }
+    p->S = S;
+    p->tree = true;
+    return TRIVANCE_OK;
+}
+
 }  // namespace
 
 namespace trivance {
@@ -134,8 +265,11 @@ int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance
         }
         if (prod != n) return TRIVANCE_EINVAL;
     }
-    for (int d = 0; d < D; ++d)
-        if (log3_exact(dims[d]) < 0) return TRIVANCE_EUNSUPPORTED;
+    bool pow3 = true;
+    for (int d = 0; d < D; ++d) pow3 = pow3 && log3_exact(dims[d]) >= 0;
+    // Sec. 4.4 (sizes that are not powers of three): rings, bandwidth-optimal variant only
+    if (!pow3 && (D != 1 || variant != TRIVANCE_BANDWIDTH_OPT || n > trivance::kMaxTreeRanks))
+        return TRIVANCE_EUNSUPPORTED;
     if (variant == TRIVANCE_BRUCK_REF && D != 1) return TRIVANCE_EUNSUPPORTED;
 
     trivance_plan_t* p = new (std::nothrow) trivance_plan_t;
@@ -143,6 +277,37 @@ int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance
     p->n = n;
     p->D = D;
     p->variant = variant;
+    if (!pow3) {
+        p->dims[0] = n;
+        p->strides[0] = 1;
+        int rc;
+        try {
+            rc = build_tree(p);
+            if (rc == TRIVANCE_OK) {
+                for (int pass = 0; pass < 2 * p->S; ++pass) {
+                    const bool rs = pass < p->S;
+                    const int k = rs ? pass : 2 * p->S - 1 - pass;
+                    Pass ps{};
+                    ps.phase = rs ? TRIVANCE_PHASE_REDUCE_SCATTER : TRIVANCE_PHASE_ALLGATHER;
+                    ps.step = k;
+                    ps.distance[0] = p->tree_dist[k];
+                    for (int c = 1; c < kMaxDims; ++c) ps.distance[c] = 1;
+                    for (int c = 0; c < kMaxDims; ++c)
+                        for (int d = 0; d < kMaxDims; ++d) ps.modulus[c][d] = 1;
+                    ps.kept_per_rank = 0;
+                    p->passes.push_back(ps);
+                }
+            }
+        } catch (const std::bad_alloc&) {
+            rc = TRIVANCE_ENOMEM;
+        }
+        if (rc != TRIVANCE_OK) {
+            delete p;
+            return rc;
+        }
+        *out = p;
+        return TRIVANCE_OK;
+    }
     int stride = 1;
     int steps_per_dim[kMaxDims] = {};
     for (int d = 0; d < D; ++d) {
@@ -221,6 +386,17 @@ int64_t trivance_pass_bytes(const trivance_plan_t* plan, int64_t elems, int dtyp
     const Pass& ps = plan->passes[pass];
     const int64_t n = plan->n;
     if (ps.phase == TRIVANCE_PHASE_LATENCY) return 2 * n * elems * w;
+    if (plan->tree) {
+        // per receiver offset (all blocks together cover elems): reduce-scatter reads its own
+        // partial and each sending child and writes once; all-gather reads once and writes to
+        // each child
+        int64_t acc = 0;
+        for (uint32_t r : plan->tree_recv[ps.step]) {
+            const int64_t kids = ((r & trivance::kFromLeft) ? 1 : 0) + ((r & trivance::kFromRight) ? 1 : 0);
+            acc += ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER ? 2 + kids : 1 + kids;
+        }
+        return acc * elems * w;
+    }
     // Every (centre rank r, kept block j) pair of the pass touches block j in three rows:
     // reduce-scatter reads own/left/right and writes own (4 accesses); all-gather reads the
     // centre and writes both peers (3 accesses). Each block index j has exactly n / 3^(t+1)

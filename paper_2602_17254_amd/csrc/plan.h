@@ -26,6 +26,16 @@ struct Pass {
 
 }  // namespace trivance
 
+namespace trivance {
+constexpr int kMaxRecv = 768;     // receivers per step of a tree plan (kernel-argument table)
+constexpr int kMaxTreeRanks = 2200;
+// Tree-plan receiver entry: bits 0..29 offset of the receiving rank from the block's owner
+// (0 <= offset < n), bit 30: a child at offset - distance sends (from the left), bit 31: a
+// child at offset + distance sends (from the right).
+constexpr uint32_t kFromLeft = 1u << 30;
+constexpr uint32_t kFromRight = 1u << 31;
+}  // namespace trivance
+
 struct trivance_plan {
     int n = 0;
     int D = 0;
@@ -34,6 +44,12 @@ struct trivance_plan {
     int dims[trivance::kMaxDims] = {};
     int strides[trivance::kMaxDims] = {};
     std::vector<trivance::Pass> passes;
+    // Rings whose size is not a power of three (bandwidth-optimal only): every block is reduced
+    // along one tree; per step, the receivers and the sides their children send from.
+    bool tree = false;
+    std::vector<int> tree_dist;                  // distance of step k
+    std::vector<std::vector<uint32_t>> tree_recv;  // receivers of step k
+    std::vector<int> tree_dirs;                  // step k: bit 0 a child sends towards +, bit 1 towards -
 };
 
 namespace trivance {

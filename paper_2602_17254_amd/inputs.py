@@ -99,6 +99,10 @@ WORKLOADS = {
         Workload("ring243_B_32MiB", (243,), "B", 8_388_608, "normal", 2, (-(2 ** 20), 2 ** 20)),
         Workload("torus27x27_B_4MiB", (27, 27), "B", 1_048_576, "normal", 3, None, True),
         Workload("torus9x9x9_B_128MiB", (9, 9, 9), "B", 33_554_432, "hash_uniform", 4, None),
+        # rings whose size is not a power of three (the paper's 8- and 64-node rings)
+        Workload("ring8_B_32MiB", (8,), "B", 8_388_608, "normal", 5, (-(2 ** 20), 2 ** 20), True,
+                 ("nonpower3",)),
+        Workload("ring64_B_8MiB", (64,), "B", 2_097_152, "normal", 6, None, True, ("nonpower3",)),
     ]
 }
 

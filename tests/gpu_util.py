@@ -4,7 +4,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from oracle import allreduce, partition, schedule
+from oracle import allreduce, nonpow3, partition, schedule
 
 VARIANT_NAMES = {"L": "latency-optimal", "B": "bandwidth-optimal"}
 
@@ -30,6 +30,8 @@ def assert_matches_oracle(got: np.ndarray, V: np.ndarray, dims, variant: str, co
     element within 4 S 2^-23 sum|v| of the fp64 sum."""
     if variant == "L":
         want = allreduce.latency_optimal(V, dims, col_seg=col_seg)
+    elif len(dims) == 1 and dims[0] >= 2 and nonpow3.levels(dims[0])[1] != 0:
+        want = nonpow3.bandwidth_optimal_ring(V, col_blk=col_blk)
     else:
         want = allreduce.bandwidth_optimal(V, dims, col_seg=col_seg, col_blk=col_blk)
     info = {}
@@ -45,7 +47,8 @@ def assert_matches_oracle(got: np.ndarray, V: np.ndarray, dims, variant: str, co
     assert rel_ok.all(), f"{what}: fp32 beyond 1e-6 relative at {np.argwhere(~rel_ok)[:5].tolist()}"
     exact = np.array_equal(got.view(np.uint32), want.view(np.uint32)) or np.array_equal(got, want)
     assert exact, f"{what}: fp32 differs in bits from the schedule-ordered oracle"
-    S = schedule.Torus(tuple(dims)).steps
+    S = len(nonpow3.distances(dims[0])) if len(dims) == 1 and dims[0] >= 2 else \
+        schedule.Torus(tuple(dims)).steps
     err = np.abs(g - allreduce.fp64_sum(V)[None, :])
     bound = allreduce.fp32_error_bound(V, S)[None, :]
     assert (err <= bound).all(), f"{what}: fp32 outside the fp64 summation bound"

@@ -131,3 +131,43 @@ def test_executor_argument_checks_without_gpu():
     assert lib.trivance_allreduce_emulated_steps(None, 9, 10, 0, p.handle, None, 1, 3) == -1
     b = T.trivance_plan((9,), "BRUCK")
     assert lib.trivance_allreduce_emulated(None, 9, 10, 0, b.handle, None) == -2
+
+
+@pytest.mark.parametrize("n", [2, 4, 5, 7, 8, 10, 20, 32, 100, 728])
+def test_nonpower3_ring_plan_matches_oracle_tree(n):
+    """Sec. 4.4 rings: the plan's passes (distances, order) and, through the per-pass byte
+    accounting, its per-step receivers and sending children equal the oracle's tree."""
+    from oracle import nonpow3
+
+    p = T.trivance_plan((n,), "B")
+    dist = nonpow3.distances(n)
+    S = len(dist)
+    assert p.num_steps == S and p.num_passes == 2 * S
+    E = 1000
+    for i in range(2 * S):
+        phase, step, dim, d = T.trivance_plan_step(p, i)
+        assert (phase, step, dim, d) == ((1 if i < S else 2), i if i < S else 2 * S - 1 - i, 0,
+                                          dist[i if i < S else 2 * S - 1 - i])
+    # oracle tree: receivers (parent offsets) and children per step, from the contribution paths
+    recv = [dict() for _ in range(S)]
+    for u in range(n):
+        for k in range(S):
+            a, b = nonpow3.position(n, u, 0, k), nonpow3.position(n, u, 0, k + 1)
+            if a != b:
+                recv[k].setdefault(b, set()).add(a)
+    for k in range(S):
+        kids = sum(len(v) for v in recv[k].values())
+        rs = T.trivance_pass_bytes(p, E, k)
+        ag = T.trivance_pass_bytes(p, E, 2 * S - 1 - k)
+        assert rs == (2 * len(recv[k]) + kids) * E * 4
+        assert ag == (len(recv[k]) + kids) * E * 4
+    # each rank forwards each block once: n - 1 child reads per block over the reduce-scatter
+    assert sum(T.trivance_pass_bytes(p, E, k) for k in range(S)) == \
+        (2 * sum(len(r) for r in recv) + (n - 1)) * E * 4
+
+
+def test_nonpower3_limits():
+    for dims, variant in [((8,), "L"), ((8,), "BRUCK"), ((8, 8), "B"), ((2201,), "B")]:
+        with pytest.raises(T.TrivanceError) as e:
+            T.trivance_plan(dims, variant)
+        assert e.value.status == -2

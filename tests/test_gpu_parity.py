@@ -188,3 +188,34 @@ def test_fill_hash_uniform_matches_host_generator():
     T.trivance_fill_hash_uniform(buf, 4)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(buf.cpu().numpy(), inputs.hash_uniform(4, E, np.arange(n), np.arange(E)))
+
+
+NONPOW3 = [(2, 100), (4, 64 * 4 * 3 + 4), (5, 999), (7, 64 * 7 * 5 + 12), (8, 64 * 8 * 4),
+           (10, 3001), (16, 64 * 16 * 2 + 8), (20, 64 * 20 * 3 + 4), (32, 64 * 32 + 20),
+           (50, 7777), (64, 64 * 64 + 4), (100, 64 * 100 + 36), (250, 64 * 250 + 4),
+           (728, 64 * 728 + 8)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "i32"])
+@pytest.mark.parametrize("n,E", NONPOW3, ids=[f"n{n}-E{E}" for n, E in NONPOW3])
+def test_parity_nonpower3_ring(n, E, dtype):
+    """Sec. 4.4 rings (bandwidth-optimal): the tree-driven kernels against the oracle."""
+    rng = np.random.default_rng(n * 7 + E)
+    _say(f"[nonpow3] n={n} E={E} dtype={dtype}")
+    if dtype == "f32":
+        V = rng.standard_normal((n, E), dtype=np.float32)
+    else:
+        V = rng.integers(-(2 ** 31), 2 ** 31 - 1, size=(n, E), dtype=np.int32)
+    got = run_hip(V, (n,), "B")
+    assert_matches_oracle(got, V, (n,), "B", what=f"ring {n} E={E} {dtype}")
+    if dtype == "i32":
+        np.testing.assert_array_equal(got, np.broadcast_to(allreduce.exact_int_sum(V), got.shape))
+
+
+@pytest.mark.parametrize("n", [4, 7, 8, 10, 32, 100])
+def test_congestion_nonpower3_ring(n):
+    import paper_2602_17254_amd as T
+
+    _say(f"[nonpow3 congestion] n={n}")
+    got = T.trivance_congestion(T.trivance_plan((n,), "B"))
+    np.testing.assert_array_equal(got, congestion.link_loads((n,), "B"))

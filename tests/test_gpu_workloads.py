@@ -117,3 +117,26 @@ def test_torus9x9x9_bandwidth_128MiB():
     assert_matches_oracle(got, Vs, w.dims, w.variant, col_seg=seg, col_blk=blk, what=w.name)
     del buf
     torch.cuda.empty_cache()
+
+
+def test_ring8_bandwidth_32MiB_nonpower3():
+    """Sec. 4.4 ring of 8 (not a power of three), compared in full, fp32 and int32."""
+    w = inputs.WORKLOADS["ring8_B_32MiB"]
+    _say(f"[workload] {w.name} f32 (full comparison)")
+    V = inputs.normal_f32(w.seed, w.n, w.elems)
+    buf = _run_full(w, V)
+    assert_matches_oracle(buf.cpu().numpy(), V, w.dims, w.variant, what=w.name)
+    _say(f"[workload] {w.name} i32 (full comparison)")
+    Vi = inputs.uniform_i32(w.int_seed, w.n, w.elems, *w.int_range)
+    assert_matches_oracle(_run_full(w, Vi).cpu().numpy(), Vi, w.dims, w.variant, what=w.name)
+    _congestion(w)
+
+
+def test_ring64_bandwidth_8MiB_nonpower3():
+    w = inputs.WORKLOADS["ring64_B_8MiB"]
+    _say(f"[workload] {w.name} f32 (column sample)")
+    V = inputs.normal_f32(w.seed, w.n, w.elems)
+    buf = _run_full(w, V)
+    _check_sampled(w, V, buf, seed=w.seed)
+    assert bool((buf[1:] == buf[0:1]).all().item())
+    _congestion(w)
