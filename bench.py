@@ -45,11 +45,17 @@ MEASURED_TRAFFIC = {
         "bytes_per_launch": 1017880551},
     ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
         "bytes_per_launch": 32569574523},
-    ("ring8_B_32MiB", "ring_tree_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
+    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
         "bytes_per_launch": 251705947},
-    ("ring64_B_8MiB", "ring_tree_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
+    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
         "bytes_per_launch": 283163090},
 }
+
+
+def _is_pow3(v):
+    while v % 3 == 0:
+        v //= 3
+    return v == 1
 
 
 def _src_sha(path):
@@ -123,7 +129,8 @@ def run_workload(w, steps, warmup, with_cpu):
     torch.cuda.synchronize()
 
     # ---- first run: result kept for the CPU-baseline comparison ----
-    budget = {"L": 2_097_152, "B": 60_000}[w.variant]
+    # about 15 s of single-core oracle work: fewer columns as the rank count grows
+    budget = {"L": 2_097_152, "B": min(60_000, (1 << 24) // w.n)}[w.variant]
     cols = _sample_for_baseline(w, min(budget, w.elems))
     if V_host is not None:
         V_cols = np.ascontiguousarray(V_host[:, cols])
@@ -161,10 +168,10 @@ def run_workload(w, steps, warmup, with_cpu):
 
     # dominant kernel: the pass type with the most total time
     phases = [T.trivance_plan_step(plan, p)[0] for p in range(P)]
-    tree = len(w.dims) == 1 and 3 ** round(np.log(w.dims[0]) / np.log(3)) != w.dims[0]
+    tree = any(not _is_pow3(s) for s in w.dims)
     names = {0: "latency_split_kernel",
-             1: "ring_tree_step_kernel<reduce>" if tree else "block_step_kernel<reduce>",
-             2: "ring_tree_step_kernel<copy>" if tree else "block_step_kernel<copy>"}
+             1: "tree_step_kernel<reduce>" if tree else "block_step_kernel<reduce>",
+             2: "tree_step_kernel<copy>" if tree else "block_step_kernel<copy>"}
     tot = {}
     for p, ph in enumerate(phases):
         tot.setdefault(ph, [0.0, 0, 0])
@@ -246,8 +253,9 @@ def copy_probe(nbytes: int, reps: int = 3) -> None:
 
 
 SWEEP_CLASSES = [((81,), "L"), ((243,), "B"), ((27, 27), "B"), ((9, 9, 9), "B"), ((8,), "B"),
-                 ((64,), "B")]
+                 ((64,), "B"), ((32, 32), "B"), ((8, 64), "B"), ((16, 16, 16), "B")]
 SWEEP_MIB = [8, 16, 32, 64, 128]
+SWEEP_MAX_RESIDENT = 150 * 2 ** 30  # 16x16x16 stops at 32 MiB per rank (128 GiB resident)
 
 
 def sweep(steps: int, warmup: int) -> None:
@@ -263,6 +271,8 @@ def sweep(steps: int, warmup: int) -> None:
         n = plan.n
         for mib in SWEEP_MIB:
             E = mib * 2 ** 20 // 4
+            if n * E * 4 > SWEEP_MAX_RESIDENT:
+                continue
             _say(f"[sweep] {'x'.join(map(str, dims))} {variant} {mib} MiB per rank")
             buf = torch.empty((n, E), dtype=torch.float32, device="cuda")
             T.trivance_fill_hash_uniform(buf, 7)

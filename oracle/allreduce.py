@@ -175,10 +175,16 @@ def bandwidth_optimal(V: np.ndarray, dims, col_seg=None, col_blk=None, rs_passes
 
 
 def allreduce(V: np.ndarray, dims, variant: str, **kw) -> np.ndarray:
-    if len(dims) == 1 and dims[0] >= 2 and nonpow3.levels(dims[0])[1] != 0:
+    if nonpow3.is_tree(dims):
         if variant != "B":
-            raise ValueError("rings whose size is not a power of three: bandwidth-optimal only")
-        return nonpow3.bandwidth_optimal_ring(V, col_blk=kw.get("col_blk"))
+            raise ValueError("sides that are not powers of three: bandwidth-optimal only")
+        if len(dims) == 1:
+            return nonpow3.bandwidth_optimal_ring(V, col_blk=kw.get("col_blk"))
+        seg, blk = kw.get("col_seg"), kw.get("col_blk")
+        if seg is None or blk is None:
+            seg, blk = partition.column_labels(V.shape[1], len(dims), V.shape[0])
+        # the gather form: equal bit for bit to the mailbox form (pinned), fast for large tori
+        return nonpow3.bandwidth_optimal_torus_columns(V, dims, seg, blk)
     if variant == "L":
         return latency_optimal(V, dims, **kw)
     if variant == "B":

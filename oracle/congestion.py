@@ -69,8 +69,11 @@ def passes_of(torus: schedule.Torus, variant: str) -> list:
 
 
 def link_loads(dims, variant: str, routing: str = "scheduled") -> np.ndarray:
-    if len(dims) == 1 and variant == "B" and dims[0] >= 2 and nonpow3.levels(dims[0])[1] != 0:
-        return nonpow3.link_loads_ring(dims[0])  # Sec. 4.4 ring; distances < n/2 either way
+    if variant == "B" and nonpow3.is_tree(dims):
+        # Sec. 4.4 trees; every distance is below half its side, so both routings agree
+        if len(dims) == 1:
+            return nonpow3.link_loads_ring(dims[0])
+        return nonpow3.link_loads_torus(dims)
     torus = schedule.Torus(tuple(dims))
     plist = passes_of(torus, variant)
     n, D = torus.n, torus.D

@@ -5,6 +5,9 @@
 // inside one dimension (Appendix E). In each pass every rank sends, for every collective, one
 // message per offset along that collective's active dimension: offsets -3^k and +3^k for
 // Trivance (Sec. 4.1), +3^k and +2*3^k for the Bruck comparison pattern (Sec. 2.4, Fig. 1).
+// With a side that is not a power of three (Sec. 4.4) a step's distance is the tree's, and a
+// rank sends towards a side only when some child of the active dimension's tree does so at that
+// step (every rank then does, the trees being the same relative to every block).
 //
 // One 64-thread workgroup handles one (pass, dimension, line) triple, a line being the ring of
 // ranks that differ only in that dimension's coordinate (dimensions with longer sides have fewer
@@ -33,9 +36,9 @@ struct CongArgs {
     int max_lines;  // lines of the dimension with the smallest side: n / min side
     int dims[kMaxDims];
     int strides[kMaxDims];
-    int distance[kMaxPasses][kMaxDims];  // per pass and collective
-    int dirs[kMaxPasses];                // Trivance passes: bit 0 messages towards +, bit 1 towards -
-    int act_dim[kMaxPasses][kMaxDims];
+    int16_t distance[kMaxPasses][kMaxDims];  // per pass and collective (at most kMaxSide / 2)
+    uint8_t dirs[kMaxPasses][kMaxDims];     // per pass and collective: bit 0 messages towards +, bit 1 towards -
+    uint8_t act_dim[kMaxPasses][kMaxDims];
 };
 
 // Direction (+1 / -1) and hop count of a message over `offset` on a ring of `side` nodes.
@@ -104,7 +107,7 @@ __global__ __launch_bounds__(64) void congestion_kernel(int64_t* __restrict__ lo
             const int off0 = a.bruck ? dist : -dist;
             const int off1 = a.bruck ? 2 * dist : dist;
             for (int m = 0; m < 2; ++m) {
-                if (!a.bruck && !(a.dirs[pass] & (m == 0 ? 2 : 1))) continue;
+                if (!a.bruck && !(a.dirs[pass][c] & (m == 0 ? 2 : 1))) continue;
                 int dir, hops;
                 route(m == 0 ? off0 : off1, side, a.shortest != 0, &dir, &hops);
                 if (hops == 0) continue;
@@ -188,16 +191,20 @@ int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topol
     for (int d = 0; d < plan->D; ++d) max_side = plan->dims[d] > max_side ? plan->dims[d] : max_side;
     for (int p = 0; p < P; ++p) {
         for (int c = 0; c < trivance::kMaxDims; ++c) {
-            a.act_dim[p][c] = plan->passes[p].dim[c];
-            a.distance[p][c] = plan->passes[p].distance[c];
+            a.act_dim[p][c] = (uint8_t)plan->passes[p].dim[c];
+            a.distance[p][c] = (int16_t)plan->passes[p].distance[c];
         }
-        a.dirs[p] = 3;
-        if (plan->tree) {
-            // a reduce-scatter step sends child -> parent; its all-gather step retraces the
-            // messages, so the directions swap
-            const int m = plan->tree_dirs[plan->passes[p].step];
-            a.dirs[p] = plan->passes[p].phase == TRIVANCE_PHASE_REDUCE_SCATTER
-                            ? m : (((m & 1) << 1) | ((m & 2) >> 1));
+        for (int c = 0; c < trivance::kMaxDims; ++c) {
+            a.dirs[p][c] = 3;
+            if (plan->tree && c < plan->D) {
+                // a reduce-scatter step sends child -> parent (every rank sends towards a side
+                // when any offset of the active dimension's tree does); its all-gather step
+                // retraces the messages, so the directions swap
+                const trivance::Pass& ps = plan->passes[p];
+                const int m = plan->trees[ps.dim[c]].dirs[ps.dim_step[c]];
+                a.dirs[p][c] = (uint8_t)(ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER
+                                             ? m : (((m & 1) << 1) | ((m & 2) >> 1)));
+            }
         }
     }
     const uint32_t grid = (uint32_t)((int64_t)P * plan->D * a.max_lines);

@@ -24,10 +24,14 @@
 // Work unit of the block steps: one wavefront handles one chunk (64 lanes x VEC x U elements) of
 // one (collective, rank, block) pair. The pair is decoded from the unit index once per wavefront
 // with wave-uniform integer arithmetic; lanes then issue 16-byte loads and stores.
+//
+// Rings and tori with a side that is not a power of three (Sec. 4.4) run the same reduce-scatter
+// and all-gather steps along one reduction tree per dimension (tree_step_kernel below).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cstdint>
+#include <cstring>
 
 #include "plan.h"
 
@@ -422,53 +426,101 @@ __global__ __launch_bounds__(kBlockThreads) void block_step_kernel(T* __restrict
 }
 
 // ---------------------------------------------------------------------------------------------
-// Ring of any size (Sec. 4.4): every block is reduced along one tree (see plan.cpp). A step lists
-// its receivers as offsets from the block's owner with the sides their children send from; the
-// reduce-scatter computes x <- (x + from_left) + from_right with absent terms skipped, the
+// Sides that are not powers of three (Sec. 4.4): every block is reduced along one tree per
+// dimension (see plan.cpp). A rank holds a partial of block j while its offset from j has not
+// been forwarded in any dimension, so the ranks working on block j in one step of collective c
+// are j + o, with o_a a receiver of the active dimension a's tree at that step (flagged with the
+// sides its children send from) and o_d, for every other d, an offset not yet forwarded in d.
+// The reduce-scatter computes x <- (x + from_left) + from_right with absent terms skipped, the
 // all-gather copies x to the children. Each rank forwards each block once, so within a step no
 // location is both read by a neighbour and written: the update is in place.
+//
+// One wave handles one chunk of 64 * VEC elements of one (collective, block, offset tuple).
+// Units are numbered collective by collective; inside a collective: chunk fastest, then the
+// offset list of dimension 0, 1, ..., then the block's coordinates (dimension 0 first).
 struct TreeArgs {
     int64_t elems;
-    int64_t G;            // granules per rank vector
+    int64_t seg_g0[kMaxTreeDims];  // first granule of segment c
+    int64_t seg_gc[kMaxTreeDims];  // granules of segment c
     int n;
-    int dist;
-    int narrow;           // 1 if n * (G + 1) < 2^31
-    int cpb;              // chunks per block
-    int nrecv;
-    uint32_t total_units;  // n * nrecv * cpb
-    FastDiv f_cpb, f_nrecv, f_n;
-    uint32_t recv[kMaxRecv];
+    int D;
+    int narrow;                    // 1 if n * (granules of a segment + 1) < 2^31
+    int cpb;                       // chunks per block (of the largest block)
+    uint32_t unit_end[kMaxTreeDims];  // collective c owns units [unit_end[c-1], unit_end[c])
+    int act[kMaxTreeDims];         // active dimension of collective c
+    int dist[kMaxTreeDims];        // its distance
+    int side[kMaxTreeDims];
+    int stride[kMaxTreeDims];
+    uint16_t lstart[kMaxTreeDims][kMaxTreeDims];  // first table entry of list (c, d)
+    FastDiv f_cpb, f_n;
+    FastDiv f_side[kMaxTreeDims];
+    FastDiv f_len[kMaxTreeDims][kMaxTreeDims];    // length of list (c, d)
+    uint32_t tab[kMaxTab];
 };
+static_assert(sizeof(TreeArgs) <= 4096, "tree-step kernel arguments above 4 KiB");
 
 template <typename T, int VEC, bool REDUCE>
-__global__ __launch_bounds__(kBlockThreads) void ring_tree_step_kernel(T* __restrict__ buf,
-                                                                        TreeArgs a) {
+__global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict__ buf,
+                                                                   TreeArgs a) {
     using V = Vec<T, VEC>;
     constexpr int kChunk = 64 * VEC;
     const int lane = threadIdx.x & 63;
     const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t wg = xcd_contiguous(blockIdx.x, gridDim.x);
     const uint32_t unit = wg * (uint32_t)kWavesPerBlock + wave;
-    if (unit >= a.total_units) return;
-    const uint32_t pair = fdiv(unit, a.f_cpb);
-    const uint32_t chunk = unit - pair * (uint32_t)a.cpb;
-    const uint32_t j = fdiv(pair, a.f_nrecv);
-    const uint32_t i = pair - j * (uint32_t)a.nrecv;
-    const uint32_t entry = a.recv[i];
-    const uint32_t off = entry & 0x3FFFFFFFu;
-    uint32_t x = j + off;
-    if (x >= (uint32_t)a.n) x -= a.n;
-    const uint32_t left = x >= (uint32_t)a.dist ? x - a.dist : x + a.n - a.dist;
-    uint32_t right = x + a.dist;
-    if (right >= (uint32_t)a.n) right -= a.n;
+    if (unit >= a.unit_end[a.D - 1]) return;
+    int c = 0;
+#pragma unroll
+    for (int i = 0; i < kMaxTreeDims - 1; ++i)
+        if (i + 1 < a.D && unit >= a.unit_end[i]) c = i + 1;
+    uint32_t rest = unit - (c > 0 ? a.unit_end[c - 1] : 0u);
+    const uint32_t q = fdiv(rest, a.f_cpb);
+    const uint32_t chunk = rest - q * (uint32_t)a.cpb;
+    rest = q;
+    uint32_t off[kMaxTreeDims];
+    uint32_t flags = 0;
+#pragma unroll
+    for (int d = 0; d < kMaxTreeDims; ++d) {
+        off[d] = 0;
+        if (d < a.D) {
+            const uint32_t qd = fdiv(rest, a.f_len[c][d]);
+            const uint32_t i = rest - qd * a.f_len[c][d].d;
+            rest = qd;
+            const uint32_t e = a.tab[a.lstart[c][d] + i];
+            off[d] = e & 0x3FFFFFFFu;
+            if (d == a.act[c]) flags = e & (kFromLeft | kFromRight);
+        }
+    }
+    uint32_t j = 0, x = 0, xa = 0;
+#pragma unroll
+    for (int d = 0; d < kMaxTreeDims; ++d) {
+        if (d < a.D) {
+            const uint32_t qd = fdiv(rest, a.f_side[d]);
+            const uint32_t jd = rest - qd * (uint32_t)a.side[d];
+            rest = qd;
+            uint32_t xd = jd + off[d];
+            if (xd >= (uint32_t)a.side[d]) xd -= a.side[d];
+            j += jd * (uint32_t)a.stride[d];
+            x += xd * (uint32_t)a.stride[d];
+            if (d == a.act[c]) xa = xd;
+        }
+    }
+    const int ad = a.act[c];
+    const uint32_t sa = (uint32_t)a.stride[ad];
+    const uint32_t dist = (uint32_t)a.dist[c];
+    const uint32_t span = (uint32_t)a.side[ad] * sa;
+    const uint32_t left = xa >= dist ? x - dist * sa : x + span - dist * sa;
+    const uint32_t right = xa + dist < (uint32_t)a.side[ad] ? x + dist * sa : x + dist * sa - span;
 
+    const int64_t g0 = a.seg_g0[c];
+    const int64_t gc = a.seg_gc[c];
     int64_t gb, ge;
     if (a.narrow) {
-        gb = fdiv(j * (uint32_t)a.G, a.f_n);
-        ge = fdiv((j + 1) * (uint32_t)a.G, a.f_n);
+        gb = g0 + fdiv(j * (uint32_t)gc, a.f_n);
+        ge = g0 + fdiv((j + 1) * (uint32_t)gc, a.f_n);
     } else {
-        gb = (int64_t)j * a.G / a.n;
-        ge = (int64_t)(j + 1) * a.G / a.n;
+        gb = g0 + (int64_t)j * gc / a.n;
+        ge = g0 + (int64_t)(j + 1) * gc / a.n;
     }
     const int64_t E = a.elems;
     const int64_t b = imin64(gb * kGranule, E);
@@ -478,8 +530,8 @@ __global__ __launch_bounds__(kBlockThreads) void ring_tree_step_kernel(T* __rest
     T* const own = buf + (int64_t)x * E + idx;
     T* const pl = buf + (int64_t)left * E + idx;
     T* const pr = buf + (int64_t)right * E + idx;
-    const bool from_left = (entry & kFromLeft) != 0;
-    const bool from_right = (entry & kFromRight) != 0;
+    const bool from_left = (flags & kFromLeft) != 0;
+    const bool from_right = (flags & kFromRight) != 0;
     if constexpr (REDUCE) {
         V acc = ld<T, VEC, true>(own);
         V l, r;
@@ -666,32 +718,57 @@ template <typename T, int VEC>
 int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
                     int pe) {
     TreeArgs a;
+    std::memset(&a, 0, sizeof(a));
     a.elems = elems;
-    a.G = (elems + kGranule - 1) / kGranule;
     a.n = p->n;
-    a.narrow = (int64_t)p->n * (a.G + 1) < ((int64_t)1 << 31) ? 1 : 0;
+    a.D = p->D;
+    int64_t max_gc = 0;
+    const int64_t G = (elems + kGranule - 1) / kGranule;
+    for (int c = 0; c < p->D; ++c) {
+        a.seg_g0[c] = (int64_t)c * G / p->D;
+        a.seg_gc[c] = (int64_t)(c + 1) * G / p->D - a.seg_g0[c];
+        max_gc = std::max(max_gc, a.seg_gc[c]);
+    }
+    a.narrow = (int64_t)p->n * (max_gc + 1) < ((int64_t)1 << 31) ? 1 : 0;
     a.f_n = make_fastdiv((uint32_t)p->n);
+    for (int d = 0; d < p->D; ++d) {
+        a.side[d] = p->dims[d];
+        a.stride[d] = p->strides[d];
+        a.f_side[d] = make_fastdiv((uint32_t)p->dims[d]);
+    }
     const int64_t max_blk = max_block_granules(p, elems) * kGranule;
     a.cpb = (int)std::max<int64_t>(1, (max_blk + 64 * VEC - 1) / (64 * VEC));
     a.f_cpb = make_fastdiv((uint32_t)a.cpb);
     for (int pi = pb; pi < pe; ++pi) {
         const Pass& ps = p->passes[pi];
-        const std::vector<uint32_t>& recv = p->tree_recv[ps.step];
-        a.dist = p->tree_dist[ps.step];
-        a.nrecv = (int)recv.size();
-        if (a.nrecv == 0) continue;
-        for (int i = 0; i < a.nrecv; ++i) a.recv[i] = recv[i];
-        a.f_nrecv = make_fastdiv((uint32_t)a.nrecv);
-        const int64_t total = (int64_t)p->n * a.nrecv * a.cpb;
-        if (total >= ((int64_t)1 << 31) - kWavesPerBlock) return TRIVANCE_EUNSUPPORTED;
-        a.total_units = (uint32_t)total;
+        int used = 0;
+        int64_t total = 0;
+        for (int c = 0; c < p->D; ++c) {
+            const int ad = ps.dim[c];
+            a.act[c] = ad;
+            a.dist[c] = ps.distance[c];
+            int64_t units = (int64_t)p->n * a.cpb;
+            for (int d = 0; d < p->D; ++d) {
+                const std::vector<uint32_t>& list =
+                    d == ad ? p->trees[d].recv[ps.dim_step[c]] : p->trees[d].alive[ps.taken[c][d]];
+                if (used + (int)list.size() > kMaxTab) return TRIVANCE_EUNSUPPORTED;
+                a.lstart[c][d] = (uint16_t)used;
+                for (uint32_t v : list) a.tab[used++] = v;
+                a.f_len[c][d] = make_fastdiv((uint32_t)std::max<size_t>(1, list.size()));
+                units *= (int64_t)list.size();
+            }
+            total += units;
+            if (total >= ((int64_t)1 << 31) - kWavesPerBlock) return TRIVANCE_EUNSUPPORTED;
+            a.unit_end[c] = (uint32_t)total;
+        }
+        if (total == 0) continue;
         const dim3 grid((uint32_t)((total + kWavesPerBlock - 1) / kWavesPerBlock));
         if (ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER)
-            hipLaunchKernelGGL((ring_tree_step_kernel<T, VEC, true>), grid, dim3(kBlockThreads),
-                               0, stream, buf, a);
+            hipLaunchKernelGGL((tree_step_kernel<T, VEC, true>), grid, dim3(kBlockThreads), 0,
+                               stream, buf, a);
         else
-            hipLaunchKernelGGL((ring_tree_step_kernel<T, VEC, false>), grid,
-                               dim3(kBlockThreads), 0, stream, buf, a);
+            hipLaunchKernelGGL((tree_step_kernel<T, VEC, false>), grid, dim3(kBlockThreads), 0,
+                               stream, buf, a);
         if (hipGetLastError() != hipSuccess) return TRIVANCE_EHIP;
     }
     return TRIVANCE_OK;

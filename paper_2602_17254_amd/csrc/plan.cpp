@@ -80,15 +80,17 @@ Pass make_pass(const trivance_plan_t* p, const Rotation& rot, int phase, int t) 
     return ps;
 }
 
-// ---- rings whose size is not a power of three (Sec. 4.4) ----
+// ---- sides that are not powers of three (Sec. 4.4) ----
 //
-// f full steps at distances 3^0..3^(f-1), then a final step at d = ceil((n - 3^f) / 2). Every
-// block j is reduced along one tree so that each rank forwards each block once (Sec. 4.4); the
-// tree is read from three ordinary Trivance trees rooted at offsets 0, +d and -d from j (offsets
-// in (-n/2, n/2]): ranks beyond j's window (|offset| > R = (3^f - 1)/2) start in the tree of
-// their side; then, until nothing changes, every rank on the path of a +/- member joins that
-// tree, and a member of j's tree whose path meets another tree joins it. The root offsets +d
-// and -d hand their partials to j in the final step.
+// A ring (or torus dimension) of side n with 3^f < n < 3^(f+1) takes f full steps at distances
+// 3^0..3^(f-1), then a final step at d = ceil((n - 3^f) / 2). Every block j is reduced along one
+// tree so that each rank forwards each block once (Sec. 4.4); the tree is read from three
+// ordinary Trivance trees rooted at offsets 0, +d and -d from j (offsets in (-n/2, n/2]): ranks
+// beyond j's window (|offset| > R = (3^f - 1)/2) start in the tree of their side; then, until
+// nothing changes, every rank on the path of a +/- member joins that tree, and a member of j's
+// tree whose path meets another tree joins it. The root offsets +d and -d hand their partials
+// to j in the final step. For n = 3^f this is the ordinary tree (d = 0, all offsets in j's
+// window): an offset sends at the step of its lowest non-zero balanced-ternary digit.
 
 // Balanced-ternary digits of v (lowest first, f of them); false if v needs more digits.
 bool balanced_digits(long v, int f, int* e) {
@@ -100,8 +102,13 @@ bool balanced_digits(long v, int f, int* e) {
     return v == 0;
 }
 
-int build_tree(trivance_plan_t* p) {
-    const int n = p->n;
+int build_dim_tree(int n, trivance::DimTree* t) {
+    t->side = n;
+    if (n == 1) {
+        t->S = 0;
+        t->alive.assign(1, std::vector<uint32_t>(1, 0u));
+        return TRIVANCE_OK;
+    }
     int f = 0;
     long pw = 1;
     while (pw * 3 <= n) {
@@ -161,7 +168,7 @@ int build_tree(trivance_plan_t* p) {
     if (fam[idx(0)] != 0) return TRIVANCE_EUNSUPPORTED;
 
     // send step, direction and parent of every offset; receivers per step
-    const int S = f + 1;
+    const int S = d ? f + 1 : f;
     std::vector<int> step(n, S), dir(n, 0);
     std::vector<long> parent(n, 0);
     for (long o = lo; o < lo + n; ++o) {
@@ -180,15 +187,18 @@ int build_tree(trivance_plan_t* p) {
                 break;
             }
         }
+        if (k >= S) return TRIVANCE_EUNSUPPORTED;
         const long dist = k < f ? pw_k : d;
         step[idx(o)] = k;
         dir[idx(o)] = ek;
         parent[idx(o)] = canon(o - ek * dist);
     }
-    p->tree_dist.assign(S, 0);
-    p->tree_dirs.assign(S, 0);
-    p->tree_recv.assign(S, std::vector<uint32_t>());
-    for (int k = 0; k < S; ++k) p->tree_dist[k] = k < f ? ipow3(k) : (int)d;
+    t->S = S;
+    t->dist.assign(S, 0);
+    t->dirs.assign(S, 0);
+    t->recv.assign(S, std::vector<uint32_t>());
+    t->alive.assign(S + 1, std::vector<uint32_t>());
+    for (int k = 0; k < S; ++k) t->dist[k] = k < f ? ipow3(k) : (int)d;
     std::vector<std::vector<uint32_t>> flags(S, std::vector<uint32_t>(n, 0));
     for (long o = lo; o < lo + n; ++o) {
         if (o == 0) continue;
@@ -196,16 +206,71 @@ int build_tree(trivance_plan_t* p) {
         const long par = parent[idx(o)];
         if (par != 0 && step[idx(par)] <= k) return TRIVANCE_EUNSUPPORTED;  // not a tree
         flags[k][idx(par)] |= dir[idx(o)] > 0 ? trivance::kFromRight : trivance::kFromLeft;
-        p->tree_dirs[k] |= dir[idx(o)] > 0 ? 2 : 1;
+        t->dirs[k] |= dir[idx(o)] > 0 ? 2 : 1;
     }
-    for (int k = 0; k < S; ++k) {
-        for (long o = lo; o < lo + n; ++o) {
-            const uint32_t fl = flags[k][idx(o)];
-            if (fl) p->tree_recv[k].push_back((uint32_t)((o % n + n) % n) | fl);
+    for (long o = lo; o < lo + n; ++o) {
+        const uint32_t res = (uint32_t)((o % n + n) % n);
+        for (int m = 0; m <= step[idx(o)]; ++m) t->alive[m].push_back(res);
+        for (int k = 0; k < S; ++k)
+            if (flags[k][idx(o)]) t->recv[k].push_back(res | flags[k][idx(o)]);
+    }
+    return TRIVANCE_OK;
+}
+
+// Tree plan: one tree per dimension; collective c at global step t takes the first dimension,
+// in cyclic order from (c + t) mod D, in which it still has steps left (the rule used for
+// unequal sides). Reduce-scatter passes t = 0..S-1, then the all-gather in reverse order.
+int build_tree_plan(trivance_plan_t* p) {
+    p->trees.assign(p->D, trivance::DimTree());
+    p->S = 0;
+    for (int dd = 0; dd < p->D; ++dd) {
+        const int rc = build_dim_tree(p->dims[dd], &p->trees[dd]);
+        if (rc != TRIVANCE_OK) return rc;
+        p->S += p->trees[dd].S;
+    }
+    if (2 * p->S > 40) return TRIVANCE_EUNSUPPORTED;
+    std::vector<Pass> rs(p->S);
+    for (int t = 0; t < p->S; ++t) {
+        rs[t] = Pass{};
+        rs[t].phase = TRIVANCE_PHASE_REDUCE_SCATTER;
+        rs[t].step = t;
+        for (int c = 0; c < kMaxDims; ++c) {
+            rs[t].distance[c] = 1;
+            for (int dd = 0; dd < kMaxDims; ++dd) rs[t].modulus[c][dd] = 1;
         }
-        if ((int)p->tree_recv[k].size() > trivance::kMaxRecv) return TRIVANCE_EUNSUPPORTED;
     }
-    p->S = S;
+    for (int c = 0; c < p->D; ++c) {
+        int count[kMaxDims] = {};
+        for (int t = 0; t < p->S; ++t) {
+            int dsel = -1;
+            for (int i = 0; i < p->D && dsel < 0; ++i) {
+                const int cand = (c + t + i) % p->D;
+                if (count[cand] < p->trees[cand].S) dsel = cand;
+            }
+            Pass& ps = rs[t];
+            ps.dim[c] = dsel;
+            ps.dim_step[c] = count[dsel];
+            ps.distance[c] = p->trees[dsel].dist[count[dsel]];
+            for (int dd = 0; dd < p->D; ++dd) ps.taken[c][dd] = count[dd];
+            count[dsel] += 1;
+        }
+    }
+    // every pass's offset lists must fit the kernel-argument table
+    for (int t = 0; t < p->S; ++t) {
+        size_t entries = 0;
+        for (int c = 0; c < p->D; ++c)
+            for (int dd = 0; dd < p->D; ++dd)
+                entries += dd == rs[t].dim[c]
+                               ? p->trees[dd].recv[rs[t].dim_step[c]].size()
+                               : p->trees[dd].alive[rs[t].taken[c][dd]].size();
+        if (entries > (size_t)trivance::kMaxTab) return TRIVANCE_EUNSUPPORTED;
+    }
+    for (int t = 0; t < p->S; ++t) p->passes.push_back(rs[t]);
+    for (int t = p->S - 1; t >= 0; --t) {
+        Pass ps = rs[t];
+        ps.phase = TRIVANCE_PHASE_ALLGATHER;
+        p->passes.push_back(ps);
+    }
     p->tree = true;
     return TRIVANCE_OK;
 }
@@ -267,9 +332,13 @@ int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance
     }
     bool pow3 = true;
     for (int d = 0; d < D; ++d) pow3 = pow3 && log3_exact(dims[d]) >= 0;
-    // Sec. 4.4 (sizes that are not powers of three): rings, bandwidth-optimal variant only
-    if (!pow3 && (D != 1 || variant != TRIVANCE_BANDWIDTH_OPT || n > trivance::kMaxTreeRanks))
-        return TRIVANCE_EUNSUPPORTED;
+    // Sec. 4.4 (sides that are not powers of three): bandwidth-optimal variant only
+    if (!pow3) {
+        if (variant != TRIVANCE_BANDWIDTH_OPT || D > trivance::kMaxTreeDims)
+            return TRIVANCE_EUNSUPPORTED;
+        for (int d = 0; d < D; ++d)
+            if (dims[d] > trivance::kMaxTreeSide) return TRIVANCE_EUNSUPPORTED;
+    }
     if (variant == TRIVANCE_BRUCK_REF && D != 1) return TRIVANCE_EUNSUPPORTED;
 
     trivance_plan_t* p = new (std::nothrow) trivance_plan_t;
@@ -278,26 +347,15 @@ int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance
     p->D = D;
     p->variant = variant;
     if (!pow3) {
-        p->dims[0] = n;
-        p->strides[0] = 1;
+        int stride1 = 1;
+        for (int d = 0; d < D; ++d) {
+            p->dims[d] = dims[d];
+            p->strides[d] = stride1;
+            stride1 *= dims[d];
+        }
         int rc;
         try {
-            rc = build_tree(p);
-            if (rc == TRIVANCE_OK) {
-                for (int pass = 0; pass < 2 * p->S; ++pass) {
-                    const bool rs = pass < p->S;
-                    const int k = rs ? pass : 2 * p->S - 1 - pass;
-                    Pass ps{};
-                    ps.phase = rs ? TRIVANCE_PHASE_REDUCE_SCATTER : TRIVANCE_PHASE_ALLGATHER;
-                    ps.step = k;
-                    ps.distance[0] = p->tree_dist[k];
-                    for (int c = 1; c < kMaxDims; ++c) ps.distance[c] = 1;
-                    for (int c = 0; c < kMaxDims; ++c)
-                        for (int d = 0; d < kMaxDims; ++d) ps.modulus[c][d] = 1;
-                    ps.kept_per_rank = 0;
-                    p->passes.push_back(ps);
-                }
-            }
+            rc = build_tree_plan(p);
         } catch (const std::bad_alloc&) {
             rc = TRIVANCE_ENOMEM;
         }
@@ -387,15 +445,26 @@ int64_t trivance_pass_bytes(const trivance_plan_t* plan, int64_t elems, int dtyp
     const int64_t n = plan->n;
     if (ps.phase == TRIVANCE_PHASE_LATENCY) return 2 * n * elems * w;
     if (plan->tree) {
-        // per receiver offset (all blocks together cover elems): reduce-scatter reads its own
-        // partial and each sending child and writes once; all-gather reads once and writes to
-        // each child
+        // Collective c's pass touches, for every block j of its segment, the ranks j + o with o
+        // a receiver offset in the active dimension and an offset not yet forwarded in every
+        // other; all blocks of a segment together cover the segment. A receiver reads its own
+        // partial and each sending child and writes once (reduce-scatter), or reads once and
+        // writes to each child (all-gather).
         int64_t acc = 0;
-        for (uint32_t r : plan->tree_recv[ps.step]) {
-            const int64_t kids = ((r & trivance::kFromLeft) ? 1 : 0) + ((r & trivance::kFromRight) ? 1 : 0);
-            acc += ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER ? 2 + kids : 1 + kids;
+        for (int c = 0; c < plan->D; ++c) {
+            const int a = ps.dim[c];
+            int64_t per = 0;
+            for (uint32_t r : plan->trees[a].recv[ps.dim_step[c]]) {
+                const int64_t kids = ((r & trivance::kFromLeft) ? 1 : 0) + ((r & trivance::kFromRight) ? 1 : 0);
+                per += ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER ? 2 + kids : 1 + kids;
+            }
+            for (int d = 0; d < plan->D; ++d)
+                if (d != a) per *= (int64_t)plan->trees[d].alive[ps.taken[c][d]].size();
+            int64_t b, e;
+            trivance::block_bounds(plan, elems, c, -1, &b, &e);
+            acc += per * (e - b);
         }
-        return acc * elems * w;
+        return acc * w;
     }
     // Every (centre rank r, kept block j) pair of the pass touches block j in three rows:
     // reduce-scatter reads own/left/right and writes own (4 accesses); all-gather reads the

@@ -22,18 +22,34 @@ struct Pass {
     // every d; the same pairs (r, j) are the senders of all-gather step t.
     int modulus[kMaxDims][kMaxDims];
     int64_t kept_per_rank;  // n / 3^(t+1): blocks kept by a rank after the step
+    // Tree plans only: the step index inside the active dimension's tree, and the number of
+    // steps collective c took in dimension d before this one.
+    int dim_step[kMaxDims];
+    int taken[kMaxDims][kMaxDims];
 };
 
 }  // namespace trivance
 
 namespace trivance {
-constexpr int kMaxRecv = 768;     // receivers per step of a tree plan (kernel-argument table)
-constexpr int kMaxTreeRanks = 2200;
-// Tree-plan receiver entry: bits 0..29 offset of the receiving rank from the block's owner
-// (0 <= offset < n), bit 30: a child at offset - distance sends (from the left), bit 31: a
-// child at offset + distance sends (from the right).
+constexpr int kMaxTab = 768;       // offset-table entries of one tree step (kernel arguments)
+constexpr int kMaxTreeSide = 2200;  // longest side of a tree plan
+constexpr int kMaxTreeDims = 4;
+// Tree-plan table entry: bits 0..29 offset of a rank from the block's owner along one dimension
+// (0 <= offset < side); on the active dimension's receivers, bit 30: a child at offset - distance
+// sends (from the left), bit 31: a child at offset + distance sends (from the right).
 constexpr uint32_t kFromLeft = 1u << 30;
 constexpr uint32_t kFromRight = 1u << 31;
+
+// The reduction tree of one dimension (Sec. 4.4 for sides that are not powers of three; the
+// ordinary balanced-ternary tree otherwise; no steps for a side of 1).
+struct DimTree {
+    int side = 1;
+    int S = 0;
+    std::vector<int> dist;                     // distance of step k
+    std::vector<std::vector<uint32_t>> recv;   // step k: receivers with the sides of their children
+    std::vector<std::vector<uint32_t>> alive;  // alive[m]: offsets not forwarded in steps < m
+    std::vector<int> dirs;                     // step k: bit 0 a child sends towards +, bit 1 towards -
+};
 }  // namespace trivance
 
 struct trivance_plan {
@@ -44,12 +60,11 @@ struct trivance_plan {
     int dims[trivance::kMaxDims] = {};
     int strides[trivance::kMaxDims] = {};
     std::vector<trivance::Pass> passes;
-    // Rings whose size is not a power of three (bandwidth-optimal only): every block is reduced
-    // along one tree; per step, the receivers and the sides their children send from.
+    // Rings and tori with a side that is not a power of three (bandwidth-optimal only): every
+    // block is reduced along one tree per dimension (trees[d]); a rank holds a partial of block j
+    // while its offset from j, in every dimension, has not yet been forwarded.
     bool tree = false;
-    std::vector<int> tree_dist;                  // distance of step k
-    std::vector<std::vector<uint32_t>> tree_recv;  // receivers of step k
-    std::vector<int> tree_dirs;                  // step k: bit 0 a child sends towards +, bit 1 towards -
+    std::vector<trivance::DimTree> trees;
 };
 
 namespace trivance {

@@ -57,7 +57,7 @@ def hash_uniform(seed: int, E: int, ranks, cols) -> np.ndarray:
 class Workload:
     """One named emulated-AllReduce workload.
 
-    dims      ring (one entry) or torus sides, all powers of three
+    dims      ring (one entry) or torus sides
     variant   'L' latency-optimal or 'B' bandwidth-optimal (reduce-scatter + all-gather)
     elems     elements per rank vector
     dist      'normal' (N(0,1) fp32 from numpy) or 'hash_uniform' (U(-1,1), generated on device)
@@ -103,6 +103,13 @@ WORKLOADS = {
         Workload("ring8_B_32MiB", (8,), "B", 8_388_608, "normal", 5, (-(2 ** 20), 2 ** 20), True,
                  ("nonpower3",)),
         Workload("ring64_B_8MiB", (64,), "B", 2_097_152, "normal", 6, None, True, ("nonpower3",)),
+        # the paper's tori whose sides are not powers of three
+        Workload("torus32x32_B_8MiB", (32, 32), "B", 2_097_152, "hash_uniform", 7, None, True,
+                 ("nonpower3",)),
+        Workload("torus8x64_B_8MiB", (8, 64), "B", 2_097_152, "hash_uniform", 8, None, True,
+                 ("nonpower3",)),
+        Workload("torus16x16x16_B_8MiB", (16, 16, 16), "B", 2_097_152, "hash_uniform", 9, None,
+                 False, ("nonpower3",)),
     ]
 }
 

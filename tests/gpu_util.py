@@ -30,8 +30,13 @@ def assert_matches_oracle(got: np.ndarray, V: np.ndarray, dims, variant: str, co
     element within 4 S 2^-23 sum|v| of the fp64 sum."""
     if variant == "L":
         want = allreduce.latency_optimal(V, dims, col_seg=col_seg)
-    elif len(dims) == 1 and dims[0] >= 2 and nonpow3.levels(dims[0])[1] != 0:
+    elif nonpow3.is_tree(dims) and len(dims) == 1:
         want = nonpow3.bandwidth_optimal_ring(V, col_blk=col_blk)
+    elif nonpow3.is_tree(dims):
+        # the gather form, equal bit for bit to the mailbox form (pinned in the oracle tests)
+        if col_seg is None or col_blk is None:
+            col_seg, col_blk = partition.column_labels(V.shape[1], len(dims), V.shape[0])
+        want = nonpow3.bandwidth_optimal_torus_columns(V, dims, col_seg, col_blk)
     else:
         want = allreduce.bandwidth_optimal(V, dims, col_seg=col_seg, col_blk=col_blk)
     info = {}
@@ -47,7 +52,7 @@ def assert_matches_oracle(got: np.ndarray, V: np.ndarray, dims, variant: str, co
     assert rel_ok.all(), f"{what}: fp32 beyond 1e-6 relative at {np.argwhere(~rel_ok)[:5].tolist()}"
     exact = np.array_equal(got.view(np.uint32), want.view(np.uint32)) or np.array_equal(got, want)
     assert exact, f"{what}: fp32 differs in bits from the schedule-ordered oracle"
-    S = len(nonpow3.distances(dims[0])) if len(dims) == 1 and dims[0] >= 2 else \
+    S = sum(nonpow3.dim_steps(int(s)) for s in dims) if nonpow3.is_tree(dims) else \
         schedule.Torus(tuple(dims)).steps
     err = np.abs(g - allreduce.fp64_sum(V)[None, :])
     bound = allreduce.fp32_error_bound(V, S)[None, :]
@@ -57,15 +62,22 @@ def assert_matches_oracle(got: np.ndarray, V: np.ndarray, dims, variant: str, co
     return info
 
 
-def sample_columns(E: int, D: int, n: int, variant: str, seed: int, per_block: int = 2):
+def sample_columns(E: int, D: int, n: int, variant: str, seed: int, per_block: int = 2,
+                   max_blocks: int | None = None):
     """Deterministic column sample of a large run: for every (segment, block) its first and last
     element and `per_block` seeded random ones (variant B), or segment ends plus random columns
-    (variant L). Returns sorted unique columns with their labels."""
+    (variant L). With max_blocks, only that many seeded blocks per segment (always including the
+    first and last) are sampled. Returns sorted unique columns with their labels."""
     rng = np.random.default_rng(seed)
     cols = []
     if variant == "B":
         for row in partition.block_bounds(E, D, n):
-            for (b, e) in row:
+            pick = range(len(row))
+            if max_blocks is not None and max_blocks < len(row):
+                pick = sorted({0, len(row) - 1} |
+                              set(rng.choice(len(row), max_blocks - 2, replace=False).tolist()))
+            for i in pick:
+                b, e = row[i]
                 if e > b:
                     cols += [b, e - 1] + rng.integers(b, e, per_block).tolist()
     else:

@@ -87,7 +87,7 @@ def test_plan_errors():
         T.trivance_plan((8,), "L")
     assert e.value.status == -2
     with pytest.raises(T.TrivanceError) as e:
-        T.trivance_plan((9, 8), "B")
+        T.trivance_plan((9, 8), "L")
     assert e.value.status == -2
     with pytest.raises(T.TrivanceError) as e:
         T.trivance_plan((9, 9), "BRUCK")
@@ -166,8 +166,49 @@ def test_nonpower3_ring_plan_matches_oracle_tree(n):
         (2 * sum(len(r) for r in recv) + (n - 1)) * E * 4
 
 
+@pytest.mark.parametrize("dims", [(4, 4), (2, 3), (8, 8), (5, 7), (3, 8), (8, 3), (1, 8),
+                                  (4, 4, 4), (2, 3, 4), (9, 2, 3), (2, 2, 2, 2)])
+def test_nonpower3_torus_plan_matches_oracle(dims):
+    """Tori with a side that is not a power of three: every pass's dimension and distance per
+    collective equal the oracle's rotation, and the per-pass bytes, which count the receivers
+    and sending children of every block's step, equal the edges of the oracle's contribution
+    paths (so the plan's receiver and not-yet-forwarded offset lists are the oracle's)."""
+    from oracle import nonpow3, partition
+
+    dims = tuple(dims)
+    D = len(dims)
+    n = int(np.prod(dims))
+    p = T.trivance_plan(dims, "B")
+    S = sum(nonpow3.dim_steps(s) for s in dims)
+    assert p.num_steps == S and p.num_passes == 2 * S
+    rot = [nonpow3.torus_rotation(dims, c) for c in range(D)]
+    for i in range(2 * S):
+        t = i if i < S else 2 * S - 1 - i
+        for c in range(D):
+            phase, step, dim, d = T.trivance_plan_step(p, i, c)
+            want_dim, k = rot[c][t]
+            assert (phase, step, dim, d) == ((1 if i < S else 2), t, want_dim,
+                                              nonpow3.distances(dims[want_dim])[k])
+    E = 64 * D * n + 37 * 64 + 5  # blocks of unequal sizes and a ragged tail
+    bounds = partition.block_bounds(E, D, n)
+    for t in range(S):
+        rs = ag = 0
+        for c in range(D):
+            for j in range(n):
+                pos = nonpow3.torus_paths(dims, j, c)
+                edges = {(pos[t][u], pos[t + 1][u]) for u in range(n)}
+                moves = {(a, b) for a, b in edges if a != b}
+                recv = {b for _, b in moves}
+                size = bounds[c][j][1] - bounds[c][j][0]
+                rs += (2 * len(recv) + len(moves)) * size
+                ag += (len(recv) + len(moves)) * size
+        assert T.trivance_pass_bytes(p, E, t) == rs * 4
+        assert T.trivance_pass_bytes(p, E, 2 * S - 1 - t) == ag * 4
+
+
 def test_nonpower3_limits():
-    for dims, variant in [((8,), "L"), ((8,), "BRUCK"), ((8, 8), "B"), ((2201,), "B")]:
+    for dims, variant in [((8,), "L"), ((8,), "BRUCK"), ((8, 8), "L"), ((2201,), "B"),
+                          ((2, 2, 2, 2, 2), "B"), ((2201, 2), "B")]:
         with pytest.raises(T.TrivanceError) as e:
             T.trivance_plan(dims, variant)
         assert e.value.status == -2

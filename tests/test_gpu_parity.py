@@ -219,3 +219,40 @@ def test_congestion_nonpower3_ring(n):
     _say(f"[nonpow3 congestion] n={n}")
     got = T.trivance_congestion(T.trivance_plan((n,), "B"))
     np.testing.assert_array_equal(got, congestion.link_loads((n,), "B"))
+
+
+# tori with a side that is not a power of three (one tree per dimension), including mixed sides,
+# a side of 1, four dimensions, empty blocks (E < 64 n D), ragged tails and the scalar path
+NONPOW3_TORI = [((4, 4), 64 * 16 * 2 * 3 + 4), ((2, 3), 101), ((8, 8), 64 * 64 * 2 + 12),
+                ((5, 7), 7777), ((3, 8), 64 * 24 * 2 * 2 + 8), ((8, 3), 3001),
+                ((1, 8), 64 * 8 * 2 + 4), ((9, 2), 64 * 18 * 2 * 3 + 4),
+                ((4, 4, 4), 64 * 64 * 3 + 20), ((2, 3, 4), 999), ((2, 2, 2, 2), 64 * 16 * 4 + 4),
+                ((10, 3, 3), 64 * 90 * 3 + 4), ((16, 16), 64 * 256 * 2 + 36), ((4, 4), 5),
+                ((8, 8), 0)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "i32"])
+@pytest.mark.parametrize("dims,E", NONPOW3_TORI, ids=[_ids(p) for p in NONPOW3_TORI])
+def test_parity_nonpower3_torus(dims, E, dtype):
+    """Tori with a side that is not a power of three (bandwidth-optimal): against the oracle."""
+    n = int(np.prod(dims))
+    rng = np.random.default_rng(n * 11 + E)
+    _say(f"[nonpow3 torus] dims={dims} E={E} dtype={dtype}")
+    if dtype == "f32":
+        V = rng.standard_normal((n, E), dtype=np.float32)
+    else:
+        V = rng.integers(-(2 ** 31), 2 ** 31 - 1, size=(n, E), dtype=np.int32)
+    got = run_hip(V, dims, "B")
+    assert_matches_oracle(got, V, dims, "B", what=f"torus {dims} E={E} {dtype}")
+    if dtype == "i32":
+        np.testing.assert_array_equal(got, np.broadcast_to(allreduce.exact_int_sum(V), got.shape))
+
+
+@pytest.mark.parametrize("dims", [(4, 4), (5, 7), (8, 3), (1, 8), (4, 4, 4), (2, 3, 4), (16, 16),
+                                  (8, 64)])
+def test_congestion_nonpower3_torus(dims):
+    import paper_2602_17254_amd as T
+
+    _say(f"[nonpow3 torus congestion] dims={dims}")
+    got = T.trivance_congestion(T.trivance_plan(dims, "B"))
+    np.testing.assert_array_equal(got, congestion.link_loads(dims, "B"))

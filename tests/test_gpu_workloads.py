@@ -140,3 +140,44 @@ def test_ring64_bandwidth_8MiB_nonpower3():
     _check_sampled(w, V, buf, seed=w.seed)
     assert bool((buf[1:] == buf[0:1]).all().item())
     _congestion(w)
+
+
+def _device_hash_workload(w, max_blocks=None):
+    """Device-generated U(-1, 1) inputs, one run, then a column sample against the oracle (the
+    gather form on the sampled columns with their block labels) and identical bits on all ranks."""
+    import paper_2602_17254_amd as T
+
+    D = len(w.dims)
+    buf = torch.empty((w.n, w.elems), dtype=torch.float32, device="cuda")
+    T.trivance_fill_hash_uniform(buf, w.seed)
+    plan = T.trivance_plan(w.dims, w.variant)
+    T.trivance_allreduce_emulated(buf, plan)
+    torch.cuda.synchronize()
+    cols, seg, blk = sample_columns(w.elems, D, w.n, w.variant, w.seed, max_blocks=max_blocks)
+    got = buf.index_select(1, torch.from_numpy(cols).cuda()).cpu().numpy()
+    Vs = inputs.hash_uniform(w.seed, w.elems, np.arange(w.n), cols)
+    assert_matches_oracle(got, Vs, w.dims, w.variant, col_seg=seg, col_blk=blk, what=w.name)
+    assert bool((buf[1:] == buf[0:1]).all().item())
+    del buf
+    torch.cuda.empty_cache()
+
+
+def test_torus32x32_bandwidth_8MiB_nonpower3():
+    w = inputs.WORKLOADS["torus32x32_B_8MiB"]
+    _say(f"[workload] {w.name} f32, device-generated inputs (column sample)")
+    _device_hash_workload(w)
+    _congestion(w)
+
+
+def test_torus8x64_bandwidth_8MiB_nonpower3():
+    w = inputs.WORKLOADS["torus8x64_B_8MiB"]
+    _say(f"[workload] {w.name} f32, device-generated inputs (column sample)")
+    _device_hash_workload(w)
+    _congestion(w)
+
+
+def test_torus16x16x16_bandwidth_8MiB_nonpower3():
+    w = inputs.WORKLOADS["torus16x16x16_B_8MiB"]
+    _say(f"[workload] {w.name} f32, device-generated inputs (column sample of 64 blocks per "
+         "segment)")
+    _device_hash_workload(w, max_blocks=64)

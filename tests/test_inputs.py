@@ -38,7 +38,7 @@ def test_hash_uniform_grid_and_range():
 def test_workload_table():
     w = inputs.WORKLOADS
     assert inputs.HEADLINE in w
-    assert [x.n for x in w.values()] == [9, 81, 243, 729, 729, 8, 64]
+    assert [x.n for x in w.values()] == [9, 81, 243, 729, 729, 8, 64, 1024, 512, 4096]
     assert w["torus9x9x9_B_128MiB"].rank_bytes == 128 * 2 ** 20
     assert w["ring81_L_8MiB"].rank_bytes == 8 * 2 ** 20
     a = inputs.normal_f32(1, 3, 10)

@@ -1,5 +1,6 @@
 """Pins of the oracle for rings whose size is not a power of three (Sec. 4.4), CPU only."""
 
+import itertools
 import json
 import math
 import os
@@ -105,3 +106,119 @@ def test_congestion_uniform_and_final_equals_distance(n):
 def test_latency_variant_rejected():
     with pytest.raises(ValueError):
         allreduce.allreduce(np.zeros((8, 4), np.float32), (8,), "L")
+
+
+# ---- tori with a side that is not a power of three ----
+
+TORI = [(4, 4), (2, 3), (8, 8), (5, 7), (3, 8), (8, 3), (4, 4, 4), (2, 3, 4), (2, 2, 2, 2)]
+
+
+@pytest.mark.parametrize("dims", TORI)
+def test_torus_int32_bruteforce_and_forwarded_once(dims):
+    """Exact integer sums on every rank, and per collective every rank forwards n - 1 blocks over
+    the reduce-scatter (each block's contributions meet along one tree of n - 1 edges, Sec. 4.4:
+    each block forwarded once per phase)."""
+    n = int(np.prod(dims))
+    rng = np.random.default_rng(n + len(dims))
+    V = rng.integers(-(2 ** 31), 2 ** 31 - 1, size=(n, 64 * len(dims) * n + 13), dtype=np.int32)
+    stats = {}
+    out = nonpow3.bandwidth_optimal_torus(V, dims, stats=stats)
+    np.testing.assert_array_equal(out, np.broadcast_to(allreduce.exact_int_sum(V), out.shape))
+    assert (stats["sent"].sum(axis=(0, 3)) == n - 1).all()
+    assert stats["sent"].shape[0] == sum(math.ceil(math.log(s, 3) - 1e-12) for s in dims)
+    np.testing.assert_array_equal(allreduce.allreduce(V, dims, "B"), out)
+
+
+@pytest.mark.parametrize("dims", [(4, 4), (5, 7), (8, 3), (2, 3, 4)])
+def test_torus_fp32_bound_and_identical_ranks(dims):
+    n = int(np.prod(dims))
+    V = np.random.default_rng(200 + n).standard_normal((n, 64 * len(dims) * n + 7),
+                                                       dtype=np.float32)
+    out = nonpow3.bandwidth_optimal_torus(V, dims)
+    assert (out == out[0:1]).all()
+    S = sum(nonpow3.dim_steps(s) for s in dims)
+    err = np.abs(out[0].astype(np.float64) - allreduce.fp64_sum(V))
+    assert (err <= allreduce.fp32_error_bound(V, S)).all()
+
+
+@pytest.mark.parametrize("dims", [(3, 3), (9, 3), (3, 9), (3, 3, 3), (1, 9)])
+def test_torus_powers_of_three_reduce_to_the_ordinary_schedule(dims):
+    """Bits and link loads equal the ordinary torus schedule (Sec. 5) when every side is 3^s."""
+    n = int(np.prod(dims))
+    V = np.random.default_rng(11 * n).standard_normal((n, 64 * len(dims) * n + 3),
+                                                      dtype=np.float32)
+    np.testing.assert_array_equal(nonpow3.bandwidth_optimal_torus(V, dims),
+                                  allreduce.bandwidth_optimal(V, dims))
+    np.testing.assert_array_equal(nonpow3.link_loads_torus(dims), congestion.link_loads(dims, "B"))
+
+
+@pytest.mark.parametrize("n", [4, 7, 8, 16])
+def test_torus_with_unit_side_is_the_ring(n):
+    """A side of 1 takes no steps: both collectives of a 1 x n torus run the ring of n on their
+    own segment, bit for bit, and a 1-dimensional torus is the ring itself."""
+    from oracle import partition
+
+    V = np.random.default_rng(n).standard_normal((n, 128 * n + 9), dtype=np.float32)
+    seg, blk = partition.column_labels(V.shape[1], 2, n)
+    np.testing.assert_array_equal(nonpow3.bandwidth_optimal_torus(V, (1, n)),
+                                  nonpow3.bandwidth_optimal_ring(V, col_blk=blk))
+    np.testing.assert_array_equal(nonpow3.bandwidth_optimal_torus(V, (n,)),
+                                  nonpow3.bandwidth_optimal_ring(V))
+    np.testing.assert_array_equal(nonpow3.link_loads_torus((n,)), nonpow3.link_loads_ring(n))
+
+
+@pytest.mark.parametrize("dims", [(4, 4), (8, 8), (5, 7), (8, 3), (4, 4, 4)])
+def test_torus_congestion_per_dimension(dims):
+    """Every pass loads only the links of the collectives' active dimensions, each used link by
+    its distance times the number of collectives working on that dimension at that step (one
+    message per rank, direction and collective), and the all-gather mirrors the reduce-scatter."""
+    D = len(dims)
+    loads = congestion.link_loads(dims, "B")
+    S = sum(nonpow3.dim_steps(s) for s in dims)
+    assert loads.shape == (2 * S, int(np.prod(dims)), 2 * D)
+    rot = [nonpow3.torus_rotation(dims, c) for c in range(D)]
+    for t in range(S):
+        for dim in range(D):
+            users = [nonpow3.distances(dims[dim])[rot[c][t][1]] for c in range(D)
+                     if rot[c][t][0] == dim]
+            for p in (t, 2 * S - 1 - t):
+                for port in (2 * dim, 2 * dim + 1):
+                    col = loads[p, :, port]
+                    sums = {sum(x for x, b in zip(users, bits) if b)
+                            for bits in itertools.product((0, 1), repeat=len(users))}
+                    assert (col == col[0]).all() and int(col[0]) in sums
+        np.testing.assert_array_equal(loads[t].sum(axis=0)[0::2] + loads[t].sum(axis=0)[1::2],
+                                      loads[2 * S - 1 - t].sum(axis=0)[0::2]
+                                      + loads[2 * S - 1 - t].sum(axis=0)[1::2])
+
+
+@pytest.mark.parametrize("dims", [(4, 4), (2, 3), (5, 7), (8, 3), (1, 8), (4, 4, 4), (2, 3, 4),
+                                  (2, 2, 2, 2), (3, 3), (9, 3), (3, 3, 3), (7,), (8,)])
+@pytest.mark.parametrize("dtype", ["f32", "i32"])
+def test_torus_gather_form_equals_mailbox_form(dims, dtype):
+    """The gather form used for thousands of ranks is the mailbox form, bit for bit (fp32 sums
+    in the same association), with the same message statistics and link loads."""
+    from oracle import partition
+
+    n = int(np.prod(dims))
+    E = 64 * len(dims) * n + 37
+    rng = np.random.default_rng(3 * n + len(dims))
+    if dtype == "f32":
+        V = rng.standard_normal((n, E), dtype=np.float32)
+    else:
+        V = rng.integers(-(2 ** 31), 2 ** 31 - 1, size=(n, E), dtype=np.int32)
+    seg, blk = partition.column_labels(E, len(dims), n)
+    a = nonpow3.bandwidth_optimal_torus_columns(V, dims, seg, blk)
+    b = nonpow3.bandwidth_optimal_torus(V, dims)
+    np.testing.assert_array_equal(a.view(np.uint32), b.view(np.uint32))
+    np.testing.assert_array_equal(nonpow3.link_loads_torus(dims, "columns"),
+                                  nonpow3.link_loads_torus(dims, "mailbox"))
+
+
+def test_rectangular_tree_torus_final_steps_share_the_long_dimension():
+    """8 x 64 under the rotation rule for unequal step counts: the side of 8 is done after two
+    steps of each collective, so both collectives take the last two steps of the side of 64
+    together (distances 9 and then 19 = ceil((64 - 27) / 2)), doubling those links' loads."""
+    loads = congestion.link_loads((8, 64), "B")
+    assert [int(loads[p].max()) for p in range(6)] == [1, 1, 3, 3, 18, 38]
+    assert (loads[5][:, 2:] == 38).all() and (loads[5][:, :2] == 0).all()
