@@ -459,16 +459,13 @@ struct TreeArgs {
 };
 static_assert(sizeof(TreeArgs) <= 4096, "tree-step kernel arguments above 4 KiB");
 
-template <typename T, int VEC, bool REDUCE>
-__global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict__ buf,
-                                                                   TreeArgs a) {
-    using V = Vec<T, VEC>;
-    constexpr int kChunk = 64 * VEC;
-    const int lane = threadIdx.x & 63;
-    const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const uint32_t wg = xcd_contiguous(blockIdx.x, gridDim.x);
-    const uint32_t unit = wg * (uint32_t)kWavesPerBlock + wave;
-    if (unit >= a.unit_end[a.D - 1]) return;
+// Decodes work unit `unit` for this lane: element offsets of the own row and of the left and right
+// neighbours along the active dimension, and the receiver's flags. False if the lane has no
+// element in the unit (past the last unit or past the block's end).
+__device__ __forceinline__ bool tree_unit(const TreeArgs& a, uint32_t unit, int lane, int chunk_elems,
+                                          int vec, int64_t* own, int64_t* left, int64_t* right,
+                                          uint32_t* flags) {
+    if (unit >= a.unit_end[a.D - 1]) return false;
     int c = 0;
 #pragma unroll
     for (int i = 0; i < kMaxTreeDims - 1; ++i)
@@ -478,7 +475,7 @@ __global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict_
     const uint32_t chunk = rest - q * (uint32_t)a.cpb;
     rest = q;
     uint32_t off[kMaxTreeDims];
-    uint32_t flags = 0;
+    uint32_t fl = 0;
 #pragma unroll
     for (int d = 0; d < kMaxTreeDims; ++d) {
         off[d] = 0;
@@ -488,7 +485,7 @@ __global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict_
             rest = qd;
             const uint32_t e = a.tab[a.lstart[c][d] + i];
             off[d] = e & 0x3FFFFFFFu;
-            if (d == a.act[c]) flags = e & (kFromLeft | kFromRight);
+            if (d == a.act[c]) fl = e & (kFromLeft | kFromRight);
         }
     }
     uint32_t j = 0, x = 0, xa = 0;
@@ -509,8 +506,8 @@ __global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict_
     const uint32_t sa = (uint32_t)a.stride[ad];
     const uint32_t dist = (uint32_t)a.dist[c];
     const uint32_t span = (uint32_t)a.side[ad] * sa;
-    const uint32_t left = xa >= dist ? x - dist * sa : x + span - dist * sa;
-    const uint32_t right = xa + dist < (uint32_t)a.side[ad] ? x + dist * sa : x + dist * sa - span;
+    const uint32_t xl = xa >= dist ? x - dist * sa : x + span - dist * sa;
+    const uint32_t xr = xa + dist < (uint32_t)a.side[ad] ? x + dist * sa : x + dist * sa - span;
 
     const int64_t g0 = a.seg_g0[c];
     const int64_t gc = a.seg_gc[c];
@@ -525,25 +522,53 @@ __global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict_
     const int64_t E = a.elems;
     const int64_t b = imin64(gb * kGranule, E);
     const int64_t e = imin64(ge * kGranule, E);
-    const int64_t idx = b + (int64_t)chunk * kChunk + (int64_t)lane * VEC;
-    if (idx >= e) return;
-    T* const own = buf + (int64_t)x * E + idx;
-    T* const pl = buf + (int64_t)left * E + idx;
-    T* const pr = buf + (int64_t)right * E + idx;
-    const bool from_left = (flags & kFromLeft) != 0;
-    const bool from_right = (flags & kFromRight) != 0;
-    if constexpr (REDUCE) {
-        V acc = ld<T, VEC, true>(own);
-        V l, r;
-        if (from_left) l = ld<T, VEC, true>(pl);
-        if (from_right) r = ld<T, VEC, true>(pr);
-        if (from_left) acc = vadd(acc, l);
-        if (from_right) acc = vadd(acc, r);
-        st<T, VEC, true>(own, acc);
-    } else {
-        const V v = ld<T, VEC, true>(own);
-        if (from_left) st<T, VEC, true>(pl, v);
-        if (from_right) st<T, VEC, true>(pr, v);
+    const int64_t idx = b + (int64_t)chunk * chunk_elems + (int64_t)lane * vec;
+    if (idx >= e) return false;
+    *own = (int64_t)x * E + idx;
+    *left = (int64_t)xl * E + idx;
+    *right = (int64_t)xr * E + idx;
+    *flags = fl;
+    return true;
+}
+
+// One unit per wave (decoded with wave-uniform arithmetic); a wave takes U consecutive units and
+// issues all their loads before the first store, which keeps more bytes in flight per wave when
+// blocks fill only part of a chunk.
+template <typename T, int VEC, int U, bool REDUCE>
+__global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict__ buf,
+                                                                   TreeArgs a) {
+    using V = Vec<T, VEC>;
+    const int lane = threadIdx.x & 63;
+    const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t wg = xcd_contiguous(blockIdx.x, gridDim.x);
+    const uint32_t first = (wg * (uint32_t)kWavesPerBlock + wave) * (uint32_t)U;
+    int64_t po[U], pl[U], pr[U];
+    uint32_t fl[U];
+    bool ok[U];
+    V vo[U], vl[U], vr[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        ok[u] = tree_unit(a, first + u, lane, 64 * VEC, VEC, &po[u], &pl[u], &pr[u], &fl[u]);
+        if (ok[u]) {
+            vo[u] = ld<T, VEC, true>(buf + po[u]);
+            if (REDUCE) {
+                if (fl[u] & kFromLeft) vl[u] = ld<T, VEC, true>(buf + pl[u]);
+                if (fl[u] & kFromRight) vr[u] = ld<T, VEC, true>(buf + pr[u]);
+            }
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        if (!ok[u]) continue;
+        if constexpr (REDUCE) {
+            V acc = vo[u];
+            if (fl[u] & kFromLeft) acc = vadd(acc, vl[u]);
+            if (fl[u] & kFromRight) acc = vadd(acc, vr[u]);
+            st<T, VEC, true>(buf + po[u], acc);
+        } else {
+            if (fl[u] & kFromLeft) st<T, VEC, true>(buf + pl[u], vo[u]);
+            if (fl[u] & kFromRight) st<T, VEC, true>(buf + pr[u], vo[u]);
+        }
     }
 }
 
@@ -714,6 +739,18 @@ int run_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t 
     return TRIVANCE_OK;
 }
 
+template <typename T, int VEC, int U>
+void launch_tree(T* buf, const TreeArgs& a, bool rs, int64_t total, hipStream_t stream) {
+    const int64_t waves = (total + U - 1) / U;
+    const dim3 grid((uint32_t)((waves + kWavesPerBlock - 1) / kWavesPerBlock));
+    if (rs)
+        hipLaunchKernelGGL((tree_step_kernel<T, VEC, U, true>), grid, dim3(kBlockThreads), 0,
+                           stream, buf, a);
+    else
+        hipLaunchKernelGGL((tree_step_kernel<T, VEC, U, false>), grid, dim3(kBlockThreads), 0,
+                           stream, buf, a);
+}
+
 template <typename T, int VEC>
 int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
                     int pe) {
@@ -737,8 +774,13 @@ int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t
         a.f_side[d] = make_fastdiv((uint32_t)p->dims[d]);
     }
     const int64_t max_blk = max_block_granules(p, elems) * kGranule;
-    a.cpb = (int)std::max<int64_t>(1, (max_blk + 64 * VEC - 1) / (64 * VEC));
+    const int64_t chunk = 64 * VEC;
+    a.cpb = (int)std::max<int64_t>(1, (max_blk + chunk - 1) / chunk);
     a.f_cpb = make_fastdiv((uint32_t)a.cpb);
+    // Four units per wave when the blocks fill less than 80% of their chunks on average (blocks
+    // of a few granules, e.g. 16 x 16 x 16 ranks at 8 MiB); one otherwise (measured on MI355X).
+    const double fill = (double)elems / ((double)p->D * p->n * a.cpb * chunk);
+    const bool four = fill < 0.8;
     for (int pi = pb; pi < pe; ++pi) {
         const Pass& ps = p->passes[pi];
         int used = 0;
@@ -758,17 +800,15 @@ int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t
                 units *= (int64_t)list.size();
             }
             total += units;
-            if (total >= ((int64_t)1 << 31) - kWavesPerBlock) return TRIVANCE_EUNSUPPORTED;
+            if (total >= ((int64_t)1 << 31) - 4096) return TRIVANCE_EUNSUPPORTED;
             a.unit_end[c] = (uint32_t)total;
         }
         if (total == 0) continue;
-        const dim3 grid((uint32_t)((total + kWavesPerBlock - 1) / kWavesPerBlock));
-        if (ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER)
-            hipLaunchKernelGGL((tree_step_kernel<T, VEC, true>), grid, dim3(kBlockThreads), 0,
-                               stream, buf, a);
+        const bool rs = ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER;
+        if (four)
+            launch_tree<T, VEC, 4>(buf, a, rs, total, stream);
         else
-            hipLaunchKernelGGL((tree_step_kernel<T, VEC, false>), grid, dim3(kBlockThreads), 0,
-                               stream, buf, a);
+            launch_tree<T, VEC, 1>(buf, a, rs, total, stream);
         if (hipGetLastError() != hipSuccess) return TRIVANCE_EHIP;
     }
     return TRIVANCE_OK;

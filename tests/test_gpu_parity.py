@@ -193,7 +193,9 @@ def test_fill_hash_uniform_matches_host_generator():
 NONPOW3 = [(2, 100), (4, 64 * 4 * 3 + 4), (5, 999), (7, 64 * 7 * 5 + 12), (8, 64 * 8 * 4),
            (10, 3001), (16, 64 * 16 * 2 + 8), (20, 64 * 20 * 3 + 4), (32, 64 * 32 + 20),
            (50, 7777), (64, 64 * 64 + 4), (100, 64 * 100 + 36), (250, 64 * 250 + 4),
-           (728, 64 * 728 + 8)]
+           (728, 64 * 728 + 8),
+           # blocks filling whole 256-element chunks: one unit per wave (the others take four)
+           (8, 8 * 256 * 3 + 4), (20, 20 * 256 * 2)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "i32"])
@@ -228,7 +230,9 @@ NONPOW3_TORI = [((4, 4), 64 * 16 * 2 * 3 + 4), ((2, 3), 101), ((8, 8), 64 * 64 *
                 ((1, 8), 64 * 8 * 2 + 4), ((9, 2), 64 * 18 * 2 * 3 + 4),
                 ((4, 4, 4), 64 * 64 * 3 + 20), ((2, 3, 4), 999), ((2, 2, 2, 2), 64 * 16 * 4 + 4),
                 ((10, 3, 3), 64 * 90 * 3 + 4), ((16, 16), 64 * 256 * 2 + 36), ((4, 4), 5),
-                ((8, 8), 0)]
+                ((8, 8), 0),
+                # blocks filling whole 256-element chunks: one unit per wave
+                ((4, 4), 2 * 16 * 256 * 2), ((2, 3, 4), 3 * 24 * 256 + 12)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "i32"])
