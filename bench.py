@@ -4,8 +4,11 @@ python bench.py [--steps K] [--warmup W] [--workload NAME | --all] [--no-cpu-bas
 
 A step is one whole emulated AllReduce (every pass of the schedule) over the workload's n rank
 vectors, which are resident in HBM before timing starts. K steps are timed back to back, bracketed
-by device synchronisation; each pass is bracketed by HIP events on the stream it runs on, which
-gives the per-launch kernel durations used for the roofline. Throughput counts the algorithmic
+by device synchronisation. Inside the timed region HIP events on the launch stream bracket each
+phase (all passes of the latency-optimal variant; the reduce-scatter and the all-gather), whose
+passes run back to back with one kernel family: group time / launches is that family's average
+launch duration, used for the roofline. One more step after the timed region brackets every pass
+with events (per-pass diagnostic only). Throughput counts the algorithmic
 bytes of the step-by-step schedule (each participating location read once and each output
 written once per pass; trivance_algorithmic_bytes).
 
@@ -36,19 +39,25 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # same counters read for a plain copy of known size), keyed by kernel, valid only for the kernel
 # source it was measured on (sha256 of the source file, first 16 hex digits).
 MEASURED_TRAFFIC = {
-    # profiles/latency_split_kernel_ring81_L_8MiB.md, profiles/block_step_kernel_*.md
-    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "eb1e7eb8c65a7a76",
-        "bytes_per_launch": 1359033977},
-    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
-        "bytes_per_launch": 3248087435},
-    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
-        "bytes_per_launch": 1017880551},
-    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
-        "bytes_per_launch": 32569574523},
-    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
-        "bytes_per_launch": 251705947},
-    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "eb1e7eb8c65a7a76",
-        "bytes_per_launch": 283163090},
+    # profiles/<kernel>_<workload>.md
+    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "6466d5aa4cfd398a",
+        "bytes_per_launch": 1359025557},
+    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
+        "bytes_per_launch": 3248092337},
+    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
+        "bytes_per_launch": 1017885847},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
+        "bytes_per_launch": 32569585513},
+    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
+        "bytes_per_launch": 251733285},
+    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
+        "bytes_per_launch": 283185125},
+    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
+        "bytes_per_launch": 2286993347},
+    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
+        "bytes_per_launch": 1550552202},
+    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
+        "bytes_per_launch": 9724287453},
 }
 
 
@@ -148,39 +157,55 @@ def run_workload(w, steps, warmup, with_cpu):
         T.trivance_allreduce_emulated(buf, plan)
     torch.cuda.synchronize()
 
-    # ---- timed region: K steps, every pass bracketed by events on the launch stream ----
+    # Passes of one phase run back to back with one kernel family (latency: every pass; reduce-
+    # scatter; all-gather), so events at the phase boundaries give each family's average launch
+    # duration (group time / launches) without a timing marker between every two kernels.
+    phases = [T.trivance_plan_step(plan, p)[0] for p in range(P)]
+    groups = []
+    for p, ph in enumerate(phases):
+        if groups and groups[-1][2] == ph:
+            groups[-1][1] = p + 1
+        else:
+            groups.append([p, p + 1, ph])
+    G = len(groups)
+
+    # ---- timed region: K steps, events at the phase boundaries on the launch stream ----
     stream = torch.cuda.current_stream()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(P + 1)] for _ in range(steps)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(G + 1)] for _ in range(steps)]
     _say(f"[bench] {w.name}: timing {steps} steps x {P} passes")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(steps):
-        for p in range(P):
-            ev[k][p].record(stream)
-            T.trivance_allreduce_emulated_steps(buf, plan, p, p + 1, stream)
-        ev[k][P].record(stream)
+        ev[k][0].record(stream)
+        for g, (pb, pe, _) in enumerate(groups):
+            T.trivance_allreduce_emulated_steps(buf, plan, pb, pe, stream)
+            ev[k][g + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per_pass_ms = np.array([[ev[k][p].elapsed_time(ev[k][p + 1]) for p in range(P)]
-                            for k in range(steps)])
+    group_ms = np.array([[ev[k][g].elapsed_time(ev[k][g + 1]) for g in range(G)]
+                         for k in range(steps)])
     ms_per_step = wall * 1e3 / steps
     value = alg_bytes / (ms_per_step * 1e-3) / 1e9
 
-    # dominant kernel: the pass type with the most total time
-    phases = [T.trivance_plan_step(plan, p)[0] for p in range(P)]
+    # ---- after the timed region: one diagnostic step with an event around every pass ----
+    pev = [torch.cuda.Event(enable_timing=True) for _ in range(P + 1)]
+    for p in range(P):
+        pev[p].record(stream)
+        T.trivance_allreduce_emulated_steps(buf, plan, p, p + 1, stream)
+    pev[P].record(stream)
+    torch.cuda.synchronize()
+    per_pass_ms = [pev[p].elapsed_time(pev[p + 1]) for p in range(P)]
+
+    # dominant kernel: the family with the most time in the timed region
     tree = any(not _is_pow3(s) for s in w.dims)
     names = {0: "latency_split_kernel",
              1: "tree_step_kernel<reduce>" if tree else "block_step_kernel<reduce>",
              2: "tree_step_kernel<copy>" if tree else "block_step_kernel<copy>"}
-    tot = {}
-    for p, ph in enumerate(phases):
-        tot.setdefault(ph, [0.0, 0, 0])
-        tot[ph][0] += per_pass_ms[:, p].sum()
-        tot[ph][1] += steps
-        tot[ph][2] += pass_bytes[p] * steps
-    dom = max(tot, key=lambda ph: tot[ph][0])
-    dom_ms = tot[dom][0] / tot[dom][1]
-    dom_bytes = tot[dom][2] / tot[dom][1]
+    dg = int(np.argmax(group_ms.sum(axis=0)))
+    pb, pe, dom = groups[dg]
+    launches = pe - pb
+    dom_ms = float(group_ms[:, dg].mean()) / launches
+    dom_bytes = sum(pass_bytes[pb:pe]) / launches
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     src = os.path.join(ROOT, "paper_2602_17254_amd", "csrc", "executor.hip")
     meas = MEASURED_TRAFFIC.get((w.name, names[dom]))
@@ -223,7 +248,7 @@ def run_workload(w, steps, warmup, with_cpu):
             "input": w.dist,
         },
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
-        "per_pass_ms": [round(float(x), 4) for x in per_pass_ms.mean(axis=0)],
+        "per_pass_ms_diagnostic": [round(float(x), 4) for x in per_pass_ms],
         "roofline": roofline,
         "cpu_baseline": None,
     }

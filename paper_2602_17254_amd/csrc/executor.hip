@@ -438,48 +438,54 @@ __global__ __launch_bounds__(kBlockThreads) void block_step_kernel(T* __restrict
 // One wave handles one chunk of 64 * VEC elements of one (collective, block, offset tuple).
 // Units are numbered collective by collective; inside a collective: chunk fastest, then the
 // offset list of dimension 0, 1, ..., then the block's coordinates (dimension 0 first).
+// DM: largest number of dimensions the arguments describe (1 for rings, kMaxTreeDims otherwise);
+// CAP: capacity of the offset table. Both only size the kernel arguments, which are copied at
+// every launch.
+template <int DM, int CAP>
 struct TreeArgs {
     int64_t elems;
-    int64_t seg_g0[kMaxTreeDims];  // first granule of segment c
-    int64_t seg_gc[kMaxTreeDims];  // granules of segment c
+    int64_t seg_g0[DM];  // first granule of segment c
+    int64_t seg_gc[DM];  // granules of segment c
     int n;
     int D;
-    int narrow;                    // 1 if n * (granules of a segment + 1) < 2^31
-    int cpb;                       // chunks per block (of the largest block)
-    uint32_t unit_end[kMaxTreeDims];  // collective c owns units [unit_end[c-1], unit_end[c])
-    int act[kMaxTreeDims];         // active dimension of collective c
-    int dist[kMaxTreeDims];        // its distance
-    int side[kMaxTreeDims];
-    int stride[kMaxTreeDims];
-    uint16_t lstart[kMaxTreeDims][kMaxTreeDims];  // first table entry of list (c, d)
+    int narrow;          // 1 if n * (granules of a segment + 1) < 2^31
+    int cpb;             // chunks per block (of the largest block)
+    uint32_t unit_end[DM];  // collective c owns units [unit_end[c-1], unit_end[c])
+    int act[DM];         // active dimension of collective c
+    int dist[DM];        // its distance
+    int side[DM];
+    int stride[DM];
+    uint16_t lstart[DM][DM];  // first table entry of list (c, d)
     FastDiv f_cpb, f_n;
-    FastDiv f_side[kMaxTreeDims];
-    FastDiv f_len[kMaxTreeDims][kMaxTreeDims];    // length of list (c, d)
-    uint32_t tab[kMaxTab];
+    FastDiv f_side[DM];
+    FastDiv f_len[DM][DM];    // length of list (c, d)
+    uint32_t tab[CAP];
 };
-static_assert(sizeof(TreeArgs) <= 4096, "tree-step kernel arguments above 4 KiB");
+static_assert(sizeof(TreeArgs<kMaxTreeDims, kMaxTab>) <= 4096,
+              "tree-step kernel arguments above 4 KiB");
 
 // Decodes work unit `unit` for this lane: element offsets of the own row and of the left and right
 // neighbours along the active dimension, and the receiver's flags. False if the lane has no
 // element in the unit (past the last unit or past the block's end).
-__device__ __forceinline__ bool tree_unit(const TreeArgs& a, uint32_t unit, int lane, int chunk_elems,
-                                          int vec, int64_t* own, int64_t* left, int64_t* right,
-                                          uint32_t* flags) {
-    if (unit >= a.unit_end[a.D - 1]) return false;
+template <int DM, int CAP>
+__device__ __forceinline__ bool tree_unit(const TreeArgs<DM, CAP>& a, uint32_t unit, int lane,
+                                          int chunk_elems, int vec, int64_t* own, int64_t* left,
+                                          int64_t* right, uint32_t* flags) {
+    if (unit >= a.unit_end[DM == 1 ? 0 : a.D - 1]) return false;
     int c = 0;
 #pragma unroll
-    for (int i = 0; i < kMaxTreeDims - 1; ++i)
+    for (int i = 0; i < DM - 1; ++i)
         if (i + 1 < a.D && unit >= a.unit_end[i]) c = i + 1;
-    uint32_t rest = unit - (c > 0 ? a.unit_end[c - 1] : 0u);
+    uint32_t rest = unit - (c > 0 ? a.unit_end[c > 0 ? c - 1 : 0] : 0u);
     const uint32_t q = fdiv(rest, a.f_cpb);
     const uint32_t chunk = rest - q * (uint32_t)a.cpb;
     rest = q;
-    uint32_t off[kMaxTreeDims];
+    uint32_t off[DM];
     uint32_t fl = 0;
 #pragma unroll
-    for (int d = 0; d < kMaxTreeDims; ++d) {
+    for (int d = 0; d < DM; ++d) {
         off[d] = 0;
-        if (d < a.D) {
+        if (DM == 1 || d < a.D) {
             const uint32_t qd = fdiv(rest, a.f_len[c][d]);
             const uint32_t i = rest - qd * a.f_len[c][d].d;
             rest = qd;
@@ -490,11 +496,14 @@ __device__ __forceinline__ bool tree_unit(const TreeArgs& a, uint32_t unit, int 
     }
     uint32_t j = 0, x = 0, xa = 0;
 #pragma unroll
-    for (int d = 0; d < kMaxTreeDims; ++d) {
-        if (d < a.D) {
-            const uint32_t qd = fdiv(rest, a.f_side[d]);
-            const uint32_t jd = rest - qd * (uint32_t)a.side[d];
-            rest = qd;
+    for (int d = 0; d < DM; ++d) {
+        if (DM == 1 || d < a.D) {
+            uint32_t jd = rest;
+            if (DM > 1) {
+                const uint32_t qd = fdiv(rest, a.f_side[d]);
+                jd = rest - qd * (uint32_t)a.side[d];
+                rest = qd;
+            }
             uint32_t xd = jd + off[d];
             if (xd >= (uint32_t)a.side[d]) xd -= a.side[d];
             j += jd * (uint32_t)a.stride[d];
@@ -502,7 +511,7 @@ __device__ __forceinline__ bool tree_unit(const TreeArgs& a, uint32_t unit, int 
             if (d == a.act[c]) xa = xd;
         }
     }
-    const int ad = a.act[c];
+    const int ad = DM == 1 ? 0 : a.act[c];
     const uint32_t sa = (uint32_t)a.stride[ad];
     const uint32_t dist = (uint32_t)a.dist[c];
     const uint32_t span = (uint32_t)a.side[ad] * sa;
@@ -534,9 +543,9 @@ __device__ __forceinline__ bool tree_unit(const TreeArgs& a, uint32_t unit, int 
 // One unit per wave (decoded with wave-uniform arithmetic); a wave takes U consecutive units and
 // issues all their loads before the first store, which keeps more bytes in flight per wave when
 // blocks fill only part of a chunk.
-template <typename T, int VEC, int U, bool REDUCE>
+template <typename T, int VEC, int U, bool REDUCE, int DM, int CAP>
 __global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict__ buf,
-                                                                   TreeArgs a) {
+                                                                   TreeArgs<DM, CAP> a) {
     using V = Vec<T, VEC>;
     const int lane = threadIdx.x & 63;
     const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -739,22 +748,33 @@ int run_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t 
     return TRIVANCE_OK;
 }
 
-template <typename T, int VEC, int U>
-void launch_tree(T* buf, const TreeArgs& a, bool rs, int64_t total, hipStream_t stream) {
+template <typename T, int VEC, int U, int DM, int CAP>
+void launch_tree(T* buf, const TreeArgs<DM, CAP>& a, bool rs, int64_t total, hipStream_t stream) {
     const int64_t waves = (total + U - 1) / U;
     const dim3 grid((uint32_t)((waves + kWavesPerBlock - 1) / kWavesPerBlock));
     if (rs)
-        hipLaunchKernelGGL((tree_step_kernel<T, VEC, U, true>), grid, dim3(kBlockThreads), 0,
-                           stream, buf, a);
+        hipLaunchKernelGGL((tree_step_kernel<T, VEC, U, true, DM, CAP>), grid, dim3(kBlockThreads),
+                           0, stream, buf, a);
     else
-        hipLaunchKernelGGL((tree_step_kernel<T, VEC, U, false>), grid, dim3(kBlockThreads), 0,
-                           stream, buf, a);
+        hipLaunchKernelGGL((tree_step_kernel<T, VEC, U, false, DM, CAP>), grid,
+                           dim3(kBlockThreads), 0, stream, buf, a);
 }
 
-template <typename T, int VEC>
-int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
-                    int pe) {
-    TreeArgs a;
+// Offset-table entries of pass `pi` (all collectives).
+size_t tree_entries(const trivance_plan_t* p, int pi) {
+    const Pass& ps = p->passes[pi];
+    size_t used = 0;
+    for (int c = 0; c < p->D; ++c)
+        for (int d = 0; d < p->D; ++d)
+            used += d == ps.dim[c] ? p->trees[d].recv[ps.dim_step[c]].size()
+                                   : p->trees[d].alive[ps.taken[c][d]].size();
+    return used;
+}
+
+template <typename T, int VEC, int DM, int CAP>
+int run_tree_impl(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
+                  int pe) {
+    TreeArgs<DM, CAP> a;
     std::memset(&a, 0, sizeof(a));
     a.elems = elems;
     a.n = p->n;
@@ -793,7 +813,7 @@ int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t
             for (int d = 0; d < p->D; ++d) {
                 const std::vector<uint32_t>& list =
                     d == ad ? p->trees[d].recv[ps.dim_step[c]] : p->trees[d].alive[ps.taken[c][d]];
-                if (used + (int)list.size() > kMaxTab) return TRIVANCE_EUNSUPPORTED;
+                if (used + (int)list.size() > CAP) return TRIVANCE_EUNSUPPORTED;
                 a.lstart[c][d] = (uint16_t)used;
                 for (uint32_t v : list) a.tab[used++] = v;
                 a.f_len[c][d] = make_fastdiv((uint32_t)std::max<size_t>(1, list.size()));
@@ -812,6 +832,23 @@ int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t
         if (hipGetLastError() != hipSuccess) return TRIVANCE_EHIP;
     }
     return TRIVANCE_OK;
+}
+
+// Rings take the one-dimensional decode; plans whose passes need at most 64 table entries take
+// the short argument block.
+template <typename T, int VEC>
+int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
+                    int pe) {
+    size_t need = 0;
+    for (int pi = pb; pi < pe; ++pi) need = std::max(need, tree_entries(p, pi));
+    if (need > (size_t)kMaxTab) return TRIVANCE_EUNSUPPORTED;
+    const bool small = need <= 64;
+    if (p->D == 1)
+        return small ? run_tree_impl<T, VEC, 1, 64>(buf, elems, p, stream, pb, pe)
+                     : run_tree_impl<T, VEC, 1, kMaxTab>(buf, elems, p, stream, pb, pe);
+    if (p->D > kMaxTreeDims) return TRIVANCE_EUNSUPPORTED;
+    return small ? run_tree_impl<T, VEC, kMaxTreeDims, 64>(buf, elems, p, stream, pb, pe)
+                 : run_tree_impl<T, VEC, kMaxTreeDims, kMaxTab>(buf, elems, p, stream, pb, pe);
 }
 
 template <typename T>
