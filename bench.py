@@ -40,24 +40,24 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # source it was measured on (sha256 of the source file, first 16 hex digits).
 MEASURED_TRAFFIC = {
     # profiles/<kernel>_<workload>.md
-    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "6466d5aa4cfd398a",
-        "bytes_per_launch": 1359025557},
-    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
-        "bytes_per_launch": 3248092337},
-    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
-        "bytes_per_launch": 1017885847},
-    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
-        "bytes_per_launch": 32569585513},
-    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
-        "bytes_per_launch": 251733285},
-    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
-        "bytes_per_launch": 283185125},
-    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
-        "bytes_per_launch": 2286993347},
-    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
-        "bytes_per_launch": 1550552202},
-    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "6466d5aa4cfd398a",
-        "bytes_per_launch": 9724287453},
+    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "ab92a2737c95ed38",
+        "bytes_per_launch": 1359039009},
+    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "ab92a2737c95ed38",
+        "bytes_per_launch": 3248077773},
+    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "ab92a2737c95ed38",
+        "bytes_per_launch": 1017872131},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "ab92a2737c95ed38",
+        "bytes_per_launch": 32569574836},
+    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "ab92a2737c95ed38",
+        "bytes_per_launch": 251707584},
+    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "ab92a2737c95ed38",
+        "bytes_per_launch": 283163168},
+    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "ab92a2737c95ed38",
+        "bytes_per_launch": 2286988951},
+    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "ab92a2737c95ed38",
+        "bytes_per_launch": 1550548727},
+    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "ab92a2737c95ed38",
+        "bytes_per_launch": 9724269907},
 }
 
 

@@ -85,10 +85,19 @@ typedef enum {
  * dimension, in cyclic order from (c + t) mod D, in which it still has steps left, at distance
  * 3^(steps it already took there). With equal sides both rules coincide.
  *
+ * Sides that are not powers of three (Sec. 4.4; bandwidth-optimal variant only): a side of s with
+ * 3^f < s < 3^(f+1) takes f steps at distances 3^0 .. 3^(f-1) and a final step at
+ * ceil((s - 3^f) / 2), so ceil(log3 s) steps; S is the sum over the sides, and the dimension of
+ * every step follows the rule for unequal sides above. The paper gives no construction of the
+ * block sets; every block is reduced along one tree per dimension, built so that each rank
+ * forwards each block once per phase (the tree of a side that is a power of three is the
+ * ordinary one). Limits: at most 4 dimensions, sides up to 2200, at most 20 steps.
+ *
  * Errors: EINVAL for out == NULL, n < 1, ndims < 0, a side < 1, product != n;
- *         EUNSUPPORTED for a side that is not a power of three (Sec. 4.4's final-step rule is not
- *         implemented), ndims > TRIVANCE_MAX_DIMS, or TRIVANCE_BRUCK_REF on more than one
- *         dimension.
+ *         EUNSUPPORTED for a side that is not a power of three with the latency-optimal or
+ *         Bruck variant (the paper does not say how whole pre-reduced vectors would avoid
+ *         counting the final step's overlap twice), beyond the limits above,
+ *         ndims > TRIVANCE_MAX_DIMS, or TRIVANCE_BRUCK_REF on more than one dimension.
  */
 int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance_plan_t** out);
 
@@ -107,7 +116,8 @@ int trivance_plan_num_passes(const trivance_plan_t* plan);
  *   phase    <- a trivance_phase
  *   step     <- global step index t (all-gather passes run t = S-1 .. 0)
  *   dim      <- torus dimension used by this collective in this pass
- *   distance <- peer distance of this collective in this pass (3^(t div D) for equal sides)
+ *   distance <- peer distance of this collective in this pass (3^(t div D) for equal sides; the
+ *               tree step's distance for a side that is not a power of three)
  * Any output pointer may be NULL. EINVAL if pass or collective is out of range.
  */
 int trivance_plan_step(const trivance_plan_t* plan, int pass, int collective, int* phase,
@@ -151,7 +161,8 @@ int64_t trivance_pass_bytes(const trivance_plan_t* plan, int64_t elems, int dtyp
  *
  * Semantics (Sec. 2.2, 4.1-4.3, 5): integer results equal the exact column sums on every rank.
  * Float results follow the schedule: each joint reduction computes (own + left) + right with
- * left the peer at -distance, in IEEE fp32 round-to-nearest-even, no fused or reordered adds.
+ * left the peer at -distance, in IEEE fp32 round-to-nearest-even, no fused or reordered adds
+ * (for sides that are not powers of three a term is skipped when no child sends from that side).
  * The latency-optimal variant leaves ranks with (legitimately) different float bits; the
  * bandwidth-optimal one leaves identical bits on every rank.
  *
@@ -180,6 +191,11 @@ int trivance_allreduce_emulated_steps(void* buffers, int n, int64_t elems, int d
  *   loads      host int64 array [passes][n][2 D]; entry [p][r][2d] counts messages crossing the
  *              link that leaves rank r towards +d in pass p, [p][r][2d+1] towards -d.
  *   loads_len  number of entries available.
+ *
+ * Every rank sends one message per collective to each peer of the active dimension; for a side
+ * that is not a power of three, only towards the sides from which some child of that
+ * dimension's tree sends in the step (all-gather steps retrace the messages, so the directions
+ * swap).
  *
  * loads == NULL returns the required length (positive). ESIZE if loads_len is too small,
  * EUNSUPPORTED for a side above 6561. Allocates and frees a temporary device buffer.
