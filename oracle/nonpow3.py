@@ -139,6 +139,17 @@ def position(n: int, u: int, j: int, k: int) -> int:
     return (u - sum(e[i] * dist[i] for i in range(k))) % n
 
 
+def _joint(parts: dict) -> np.ndarray:
+    """Joint reduction of what a rank holds for one block after a step: (own + from_left) +
+    from_right, absent terms skipped (Sec. 4.3 reduces both messages with the local partial)."""
+    acc = None
+    for side in ("own", "left", "right"):
+        if side in parts:
+            acc = parts[side].copy() if acc is None else np.add(acc, parts[side],
+                                                                 dtype=parts[side].dtype)
+    return acc
+
+
 def bandwidth_optimal_ring(V: np.ndarray, col_blk=None, stats=None) -> np.ndarray:
     """Reduce-scatter + all-gather on a ring of any size n >= 2 (mailbox emulation).
 
@@ -184,11 +195,7 @@ def bandwidth_optimal_ring(V: np.ndarray, col_blk=None, stats=None) -> np.ndarra
         for x in range(n):
             new = {}
             for key, parts in inbox[x].items():
-                acc = None
-                for side in ("own", "left", "right"):
-                    if side in parts:
-                        acc = parts[side].copy() if acc is None else \
-                            np.add(acc, parts[side], dtype=V.dtype)
+                acc = _joint(parts)
                 if (key[0], key[1]) in new:
                     raise AssertionError("duplicate partial")
                 new[key] = acc
@@ -374,12 +381,7 @@ def bandwidth_optimal_torus(V: np.ndarray, dims, col_seg=None, col_blk=None,
             for x in range(n):
                 new = {}
                 for key, parts in inbox[x].items():
-                    acc = None
-                    for side in ("own", "left", "right"):
-                        if side in parts:
-                            acc = parts[side].copy() if acc is None else \
-                                np.add(acc, parts[side], dtype=V.dtype)
-                    new[key] = acc
+                    new[key] = _joint(parts)
                 held[x] = new
         done = tuple(() for _ in range(D))
         for x in range(n):
@@ -458,6 +460,12 @@ def _tree_tables(side: int):
     return send, digit
 
 
+def _gather_joint(own, left, right, from_left, from_right):
+    """(own + from_left) + from_right, where a child sends (the gather form of _joint)."""
+    acc = np.where(from_left, np.add(own, left, dtype=own.dtype), own)
+    return np.where(from_right, np.add(acc, right, dtype=own.dtype), acc)
+
+
 def bandwidth_optimal_torus_columns(V: np.ndarray, dims, col_seg, col_blk,
                                     stats=None) -> np.ndarray:
     """The schedule of bandwidth_optimal_torus, executed column by column in gather form: at
@@ -514,8 +522,7 @@ def bandwidth_optimal_torus_columns(V: np.ndarray, dims, col_seg, col_blk,
             recv = from_left | from_right
             if not (alive[recv].all() and (e[recv] == 0).all()):
                 raise AssertionError("a receiver is not holding its own partial")
-            acc = np.where(from_left, np.add(Q, Q[L], dtype=Q.dtype), Q)
-            Q = np.where(from_right, np.add(acc, Q[R], dtype=Q.dtype), acc)
+            Q = _gather_joint(Q, Q[L], Q[R], from_left, from_right)
         for t in reversed(range(len(rot))):
             dim, dist, alive, e = state(t)
             L, R = neighbour(dim, -dist), neighbour(dim, +dist)
