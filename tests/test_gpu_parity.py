@@ -117,14 +117,13 @@ def test_step_hook_coverage(dims):
     assert (buf.cpu().numpy()[:, [c * n * 64 + u for c in range(D) for u in range(n)]] == 1).all()
 
 
-@pytest.mark.parametrize("dims", [(27,), (9, 9)])
+@pytest.mark.parametrize("dims", [(27,), (9, 9), (8,), (64,), (4, 4), (3, 8), (2, 3, 4)])
 def test_step_hook_reduce_scatter_then_resume(dims):
     """After the reduce-scatter passes alone, rank r's block r is final (int32 exact sum);
     resuming with the all-gather passes completes the AllReduce."""
     import paper_2602_17254_amd as T
 
-    t = schedule.Torus(dims)
-    n, D = t.n, t.D
+    n, D = int(np.prod(dims)), len(dims)
     E = 64 * n * 2 + 4
     rng = np.random.default_rng(41)
     V = rng.integers(-1000, 1000, size=(n, E), dtype=np.int32)
@@ -144,6 +143,44 @@ def test_step_hook_reduce_scatter_then_resume(dims):
     T.trivance_allreduce_emulated_steps(buf, plan, S, 2 * S)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(buf.cpu().numpy(), np.broadcast_to(total, (n, E)))
+
+
+@pytest.mark.parametrize("dims", [(7,), (8,), (10,), (32,), (4, 4), (3, 8), (5, 2), (2, 3, 4)])
+def test_step_hook_tree_partials(dims):
+    """Sides that are not powers of three, one pass at a time: after reduce-scatter step t every
+    rank that still holds a partial of block j holds exactly the int32 sum of the contributions
+    whose paths (oracle) have reached it; the all-gather then leaves the exact sum everywhere."""
+    import paper_2602_17254_amd as T
+    from oracle import nonpow3
+
+    n, D = int(np.prod(dims)), len(dims)
+    E = 64 * n * D + 20
+    rng = np.random.default_rng(43 + n)
+    V = rng.integers(-(2 ** 31), 2 ** 31 - 1, size=(n, E), dtype=np.int32)
+    plan = T.trivance_plan(dims, "B")
+    S = plan.num_steps
+    bb = partition.block_bounds(E, D, n)
+    paths = {(c, j): nonpow3.torus_paths(dims, j, c) for c in range(D) for j in range(n)}
+    buf = torch.from_numpy(V).cuda()
+    for t in range(S):
+        _say(f"[tree-partials] dims={dims} step={t}")
+        T.trivance_allreduce_emulated_steps(buf, plan, t, t + 1)
+        torch.cuda.synchronize()
+        mid = buf.cpu().numpy()
+        for c in range(D):
+            for j in range(n):
+                b, e = bb[c][j]
+                pos = paths[(c, j)][t + 1]
+                for x in set(pos):
+                    want = np.zeros(e - b, dtype=np.int64)
+                    for u in range(n):
+                        if pos[u] == x:
+                            want += V[u, b:e]
+                    np.testing.assert_array_equal(mid[x, b:e], want.astype(np.int32))
+    T.trivance_allreduce_emulated_steps(buf, plan, S, 2 * S)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(buf.cpu().numpy(),
+                                  np.broadcast_to(allreduce.exact_int_sum(V), (n, E)))
 
 
 @pytest.mark.parametrize("dims,variant,routing", [
