@@ -101,10 +101,26 @@ def cpu_baseline(w, gpu_first_result_cols, cols, V_cols, seconds_target=15.0):
         "unit": "GB/s",
         "cores": 1,
         "kind": "oracle",
+        "host": _host_cpu(),
         "sample": f"{ncols} of {w.elems} columns x {w.n} ranks (all passes), {dt:.2f} s",
         "seconds": round(dt, 3),
         "matches_gpu_on_sample": same,
     }
+
+
+def _host_cpu():
+    """CPUs of the host the baseline ran on (the oracle itself uses one core)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "os_cpu_count": os.cpu_count(),
+            "affinity": len(os.sched_getaffinity(0))}
 
 
 def _sample_for_baseline(w, budget_cols):
@@ -248,6 +264,9 @@ def run_workload(w, steps, warmup, with_cpu):
             "input": w.dist,
         },
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
+        "step_ms_events": {"median": round(float(np.median(group_ms.sum(axis=1))), 4),
+                           "min": round(float(group_ms.sum(axis=1).min()), 4),
+                           "max": round(float(group_ms.sum(axis=1).max()), 4)},
         "per_pass_ms_diagnostic": [round(float(x), 4) for x in per_pass_ms],
         "roofline": roofline,
         "cpu_baseline": None,

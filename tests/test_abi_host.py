@@ -208,7 +208,7 @@ def test_nonpower3_torus_plan_matches_oracle(dims):
 
 def test_nonpower3_limits():
     for dims, variant in [((8,), "L"), ((8,), "BRUCK"), ((8, 8), "L"), ((2201,), "B"),
-                          ((2, 2, 2, 2, 2), "B"), ((2201, 2), "B")]:
+                          ((2, 2, 2, 2, 2), "B"), ((2201, 2), "B"), ((1000, 1000, 1000), "B")]:
         with pytest.raises(T.TrivanceError) as e:
             T.trivance_plan(dims, variant)
         assert e.value.status == -2

@@ -290,10 +290,14 @@ def test_parity_nonpower3_torus(dims, E, dtype):
 
 
 @pytest.mark.parametrize("dims", [(4, 4), (5, 7), (8, 3), (1, 8), (4, 4, 4), (2, 3, 4), (16, 16),
-                                  (8, 64)])
+                                  (8, 64), (2,), (2, 2)])
 def test_congestion_nonpower3_torus(dims):
+    """Both routings: every tree distance is at most half its side (a tie at exactly half keeps
+    the offset's sign), so shortest-path routing counts what scheduled routing counts."""
     import paper_2602_17254_amd as T
 
     _say(f"[nonpow3 torus congestion] dims={dims}")
-    got = T.trivance_congestion(T.trivance_plan(dims, "B"))
-    np.testing.assert_array_equal(got, congestion.link_loads(dims, "B"))
+    plan = T.trivance_plan(dims, "B")
+    want = congestion.link_loads(dims, "B")
+    np.testing.assert_array_equal(T.trivance_congestion(plan), want)
+    np.testing.assert_array_equal(T.trivance_congestion(plan, "shortest"), want)
