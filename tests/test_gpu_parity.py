@@ -75,17 +75,20 @@ def test_parity_small(shape, dtype, variant):
         np.testing.assert_array_equal(got, np.broadcast_to(allreduce.exact_int_sum(V), got.shape))
 
 
-def test_misaligned_rows_use_scalar_path():
-    """A [n, E] view whose start is not 16-byte aligned still gives the oracle's result."""
+@pytest.mark.parametrize("dims,variants", [((9,), "LB"), ((8,), "B"), ((4, 4), "B")])
+def test_misaligned_rows_use_scalar_path(dims, variants):
+    """A [n, E] view whose start is not 16-byte aligned still gives the oracle's result (block,
+    latency and tree steps)."""
     import paper_2602_17254_amd as T
 
-    dims, E = (9,), 64 * 9 * 2 + 8
+    n = int(np.prod(dims))
+    E = 64 * n * len(dims) * 2 + 8
     rng = np.random.default_rng(3)
-    V = rng.standard_normal((9, E), dtype=np.float32)
-    for variant in ("L", "B"):
-        _say(f"[misaligned] variant={variant}")
-        flat = torch.zeros(9 * E + 1, dtype=torch.float32, device="cuda")
-        view = flat[1:].view(9, E)
+    V = rng.standard_normal((n, E), dtype=np.float32)
+    for variant in variants:
+        _say(f"[misaligned] dims={dims} variant={variant}")
+        flat = torch.zeros(n * E + 1, dtype=torch.float32, device="cuda")
+        view = flat[1:].view(n, E)
         view.copy_(torch.from_numpy(V))
         assert view.data_ptr() % 16 != 0
         T.trivance_allreduce_emulated(view, T.trivance_plan(dims, variant))
