@@ -17,6 +17,9 @@ allreduce   message-passing emulation of both variants, step by step, with an ex
             barrier between posting and reducing (Sec. 4.1, 4.2, 4.3, 5), plus reference sums.
 congestion  hop-by-hop link-load walk (cost model of Sec. 2.1) and the transmission-delay
             factors of Tables 1 and 2 / Appendix B.
+nonpow3     rings and tori whose sides are not all powers of three (Sec. 4.4): the final-step
+            distance, the reduction tree of every side, a mailbox emulation of the bandwidth-
+            optimal variant and a column-by-column gather form of it, and their link loads.
 
 Parity status: every function here is pinned by a `-m "not gpu"` test against values the paper
 prints, closed forms or brute force, except the floating-point summation order of the joint

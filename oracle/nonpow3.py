@@ -1,4 +1,4 @@
-"""Trivance on rings whose size is not a power of three (oracle side, Sec. 4.4).
+"""Trivance on rings and tori whose sides are not all powers of three (oracle side, Sec. 4.4).
 
 Test infrastructure only (see the package docstring).
 
@@ -25,6 +25,8 @@ Reading (the paper gives no construction). For a block j, offsets are taken in (
   This makes every block a single tree: each rank forwards each block exactly once.
   * A rank combines what arrives for a block as (own + from_left) + from_right, absent terms
     skipped; the all-gather retraces each tree edge backwards (reverse step order).
+On a torus every side gets its own tree of this kind (the ordinary one for a power of three); see
+the section on tori below.
 """
 
 from __future__ import annotations

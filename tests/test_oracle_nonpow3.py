@@ -1,4 +1,5 @@
-"""Pins of the oracle for rings whose size is not a power of three (Sec. 4.4), CPU only."""
+"""Pins of the oracle for rings and tori whose sides are not all powers of three (Sec. 4.4), CPU
+only."""
 
 import itertools
 import json
