@@ -24,7 +24,10 @@ nonpow3     rings and tori whose sides are not all powers of three (Sec. 4.4): t
 Parity status: every function here is pinned by a `-m "not gpu"` test against values the paper
 prints, closed forms or brute force, except the floating-point summation order of the joint
 reduction, which the paper leaves open; that order is a stated reading (own + left) + right,
-pinned only through the invariants listed in tests/test_oracle_allreduce.py.
+pinned only through the invariants listed in tests/test_oracle_allreduce.py. The reduction trees
+of sides that are not powers of three are a reading too (nonpow3): integer sums, forwarding
+counts, the 7-node figure, the final-step congestion and agreement with the ordinary schedule on
+powers of three pin them; the fp32 association they produce beyond that is parity unpinned.
 """
 
 from . import schedule, partition, allreduce, congestion  # noqa: F401
