@@ -212,3 +212,53 @@ def test_nonpower3_limits():
         with pytest.raises(T.TrivanceError) as e:
             T.trivance_plan(dims, variant)
         assert e.value.status == -2
+
+
+def _random_shapes(seed, count, max_n):
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        D = int(rng.integers(1, 4))
+        dims = tuple(int(x) for x in rng.integers(1, 14 if D > 1 else 200, size=D))
+        n = int(np.prod(dims))
+        if 2 <= n <= max_n and dims not in out:
+            out.append(dims)
+    return out
+
+
+@pytest.mark.parametrize("dims", _random_shapes(11, 30, 300))
+def test_plan_matches_oracle_on_seeded_random_shapes(dims):
+    """Seeded random rings and tori, with sides that are and are not powers of three: passes,
+    distances and per-pass bytes of the bandwidth-optimal plan against the oracle's contribution
+    paths (tree plans) or its schedule and the 3.5 w E (n - 1) total (powers of three)."""
+    from oracle import nonpow3, partition
+
+    D = len(dims)
+    n = int(np.prod(dims))
+    p = T.trivance_plan(dims, "B")
+    E = 64 * D * n + 23 * 64 + 7
+    if not nonpow3.is_tree(dims):
+        assert T.trivance_algorithmic_bytes(p, E) * 2 == 7 * 4 * E * (n - 1)
+        return
+    S = sum(nonpow3.dim_steps(s) for s in dims)
+    assert p.num_passes == 2 * S
+    rot = [nonpow3.torus_rotation(dims, c) for c in range(D)]
+    for t in range(S):
+        for c in range(D):
+            _, step, dim, d = T.trivance_plan_step(p, t, c)
+            assert (step, dim, d) == (t, rot[c][t][0], nonpow3.distances(dims[rot[c][t][0]])[rot[c][t][1]])
+    bounds = partition.block_bounds(E, D, n)
+    rs = [0] * S
+    ag = [0] * S
+    for c in range(D):
+        for j in range(n):
+            pos = nonpow3.torus_paths(dims, j, c)
+            size = bounds[c][j][1] - bounds[c][j][0]
+            for t in range(S):
+                moves = {(a, b) for a, b in zip(pos[t], pos[t + 1]) if a != b}
+                recv = {b for _, b in moves}
+                rs[t] += (2 * len(recv) + len(moves)) * size
+                ag[t] += (len(recv) + len(moves)) * size
+    for t in range(S):
+        assert T.trivance_pass_bytes(p, E, t) == rs[t] * 4
+        assert T.trivance_pass_bytes(p, E, 2 * S - 1 - t) == ag[t] * 4

@@ -304,3 +304,40 @@ def test_congestion_nonpower3_torus(dims):
     want = congestion.link_loads(dims, "B")
     np.testing.assert_array_equal(T.trivance_congestion(plan), want)
     np.testing.assert_array_equal(T.trivance_congestion(plan, "shortest"), want)
+
+
+def _seeded_shapes(seed, count, max_n):
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        D = int(rng.integers(1, 4))
+        dims = tuple(int(x) for x in rng.integers(1, 12 if D > 1 else 250, size=D))
+        n = int(np.prod(dims))
+        E = int(rng.integers(1, 64 * D * n * 3))
+        if 2 <= n <= max_n and dims not in [d for d, _ in out]:
+            out.append((dims, E))
+    return out
+
+
+SEEDED = _seeded_shapes(2026, 24, 200)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "i32"])
+@pytest.mark.parametrize("dims,E", SEEDED, ids=[_ids(p) for p in SEEDED])
+def test_parity_seeded_random_shapes(dims, E, dtype):
+    """Seeded random rings and tori (sides that are and are not powers of three, 1-3 dimensions,
+    random E: vector and scalar paths, empty blocks, ragged tails), bandwidth-optimal, and the
+    latency-optimal variant where every side is a power of three."""
+    from oracle import nonpow3
+
+    n = int(np.prod(dims))
+    rng = np.random.default_rng(n + E)
+    if dtype == "f32":
+        V = rng.standard_normal((n, E), dtype=np.float32)
+    else:
+        V = rng.integers(-(2 ** 31), 2 ** 31 - 1, size=(n, E), dtype=np.int32)
+    variants = "B" if nonpow3.is_tree(dims) else "LB"
+    for variant in variants:
+        _say(f"[seeded] dims={dims} E={E} {dtype} {variant}")
+        got = run_hip(V, dims, variant)
+        assert_matches_oracle(got, V, dims, variant, what=f"{dims} E={E} {dtype} {variant}")
