@@ -96,6 +96,11 @@ def cpu_baseline(w, gpu_first_result_cols, cols, V_cols, seconds_target=15.0):
     sample_bytes = T.trivance_algorithmic_bytes(T.trivance_plan(w.dims, w.variant), w.elems) \
         * ncols / w.elems
     same = bool(np.array_equal(out, gpu_first_result_cols))
+    # the GPU's fp32 result on the sample against the fp64 sum: largest |error| / bound, where the
+    # bound is 4 S 2^-23 sum|v| (S = steps); below 1 means within the bound
+    S = T.trivance_plan(w.dims, w.variant).num_steps
+    err = np.abs(gpu_first_result_cols.astype(np.float64) - allreduce.fp64_sum(V_cols)[None, :])
+    margin = float((err / np.maximum(allreduce.fp32_error_bound(V_cols, S)[None, :], 1e-300)).max())
     return {
         "value": round(sample_bytes / dt / 1e9, 4),
         "unit": "GB/s",
@@ -105,6 +110,7 @@ def cpu_baseline(w, gpu_first_result_cols, cols, V_cols, seconds_target=15.0):
         "sample": f"{ncols} of {w.elems} columns x {w.n} ranks (all passes), {dt:.2f} s",
         "seconds": round(dt, 3),
         "matches_gpu_on_sample": same,
+        "gpu_fp64_bound_ratio_on_sample": round(margin, 4),
     }
 
 
