@@ -30,7 +30,7 @@ def assert_matches_oracle(got: np.ndarray, V: np.ndarray, dims, variant: str, co
     element within 4 S 2^-23 sum|v| of the fp64 sum."""
     if variant == "L":
         want = allreduce.latency_optimal(V, dims, col_seg=col_seg)
-    elif nonpow3.is_tree(dims) and len(dims) == 1:
+    elif nonpow3.is_tree(dims) and len(dims) == 1 and dims[0] <= 300:
         want = nonpow3.bandwidth_optimal_ring(V, col_blk=col_blk)
     elif nonpow3.is_tree(dims):
         # the gather form, equal bit for bit to the mailbox form (pinned in the oracle tests)

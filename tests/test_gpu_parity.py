@@ -341,3 +341,30 @@ def test_parity_seeded_random_shapes(dims, E, dtype):
         _say(f"[seeded] dims={dims} E={E} {dtype} {variant}")
         got = run_hip(V, dims, variant)
         assert_matches_oracle(got, V, dims, variant, what=f"{dims} E={E} {dtype} {variant}")
+
+
+@pytest.mark.parametrize("n", [1000, 2200])
+def test_parity_largest_rings_sampled(n):
+    """Rings up to the 2200-rank limit (receiver tables of several hundred entries per step):
+    int32 and fp32 on a column sample (first, last and two random elements of every block)
+    against the oracle's gather form, which equals the mailbox form bit for bit."""
+    import paper_2602_17254_amd as T
+    from gpu_util import sample_columns
+
+    E = 64 * n * 2 + 12
+    plan = T.trivance_plan((n,), "B")
+    cols, seg, blk = sample_columns(E, 1, n, "B", seed=n)
+    for dtype in ("i32", "f32"):
+        _say(f"[large ring] n={n} E={E} {dtype}")
+        rng = np.random.default_rng(n + 7)
+        if dtype == "f32":
+            V = rng.standard_normal((n, E), dtype=np.float32)
+        else:
+            V = rng.integers(-(2 ** 31), 2 ** 31 - 1, size=(n, E), dtype=np.int32)
+        buf = torch.from_numpy(V).cuda()
+        T.trivance_allreduce_emulated(buf, plan)
+        torch.cuda.synchronize()
+        got = buf.index_select(1, torch.from_numpy(cols).cuda()).cpu().numpy()
+        assert_matches_oracle(got, np.ascontiguousarray(V[:, cols]), (n,), "B", col_seg=seg,
+                              col_blk=blk, what=f"ring {n} {dtype}")
+        del buf
