@@ -797,10 +797,14 @@ int run_tree_impl(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t s
     const int64_t chunk = 64 * VEC;
     a.cpb = (int)std::max<int64_t>(1, (max_blk + chunk - 1) / chunk);
     a.f_cpb = make_fastdiv((uint32_t)a.cpb);
-    // Four units per wave when the blocks fill less than 80% of their chunks on average (blocks
-    // of a few granules, e.g. 16 x 16 x 16 ranks at 8 MiB); one otherwise (measured on MI355X).
+    // Units per wave, measured on MI355X over rings and 2- to 4-dimensional tori: the
+    // reduce-scatter takes four when the blocks fill less than 80% of their chunks on average
+    // (blocks of a few granules, e.g. 16 x 16 x 16 ranks at 8 MiB) and one otherwise; the
+    // all-gather (one load per unit) takes eight on tori of three or more dimensions whose blocks
+    // average under 4096 elements, and otherwise follows the reduce-scatter rule.
     const double fill = (double)elems / ((double)p->D * p->n * a.cpb * chunk);
-    const bool four = fill < 0.8;
+    const int u_rs = fill < 0.8 ? 4 : 1;
+    const int u_ag = (p->D >= 3 && elems < (int64_t)4096 * p->D * p->n) ? 8 : u_rs;
     for (int pi = pb; pi < pe; ++pi) {
         const Pass& ps = p->passes[pi];
         int used = 0;
@@ -825,10 +829,11 @@ int run_tree_impl(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t s
         }
         if (total == 0) continue;
         const bool rs = ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER;
-        if (four)
-            launch_tree<T, VEC, 4>(buf, a, rs, total, stream);
-        else
-            launch_tree<T, VEC, 1>(buf, a, rs, total, stream);
+        switch (rs ? u_rs : u_ag) {
+            case 8: launch_tree<T, VEC, 8>(buf, a, rs, total, stream); break;
+            case 4: launch_tree<T, VEC, 4>(buf, a, rs, total, stream); break;
+            default: launch_tree<T, VEC, 1>(buf, a, rs, total, stream); break;
+        }
         if (hipGetLastError() != hipSuccess) return TRIVANCE_EHIP;
     }
     return TRIVANCE_OK;

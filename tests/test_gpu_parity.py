@@ -272,7 +272,10 @@ NONPOW3_TORI = [((4, 4), 64 * 16 * 2 * 3 + 4), ((2, 3), 101), ((8, 8), 64 * 64 *
                 ((10, 3, 3), 64 * 90 * 3 + 4), ((16, 16), 64 * 256 * 2 + 36), ((4, 4), 5),
                 ((8, 8), 0),
                 # blocks filling whole 256-element chunks: one unit per wave
-                ((4, 4), 2 * 16 * 256 * 2), ((2, 3, 4), 3 * 24 * 256 + 12)]
+                ((4, 4), 2 * 16 * 256 * 2), ((2, 3, 4), 3 * 24 * 256 + 12),
+                # three dimensions with blocks of at least 4096 elements: one unit per wave in
+                # the all-gather (eight below that)
+                ((2, 2, 2), 3 * 8 * 4096 + 192)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "i32"])
