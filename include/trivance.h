@@ -91,7 +91,8 @@ typedef enum {
  * every step follows the rule for unequal sides above. The paper gives no construction of the
  * block sets; every block is reduced along one tree per dimension, built so that each rank
  * forwards each block once per phase (the tree of a side that is a power of three is the
- * ordinary one). Limits: at most 4 dimensions, sides up to 2200, at most 20 steps.
+ * ordinary one). Limits: at most 4 dimensions, sides up to 2200, at most 20 steps, and at most
+ * 768 offset-table entries per step (the lists travel in kernel arguments).
  *
  * Errors: EINVAL for out == NULL, n < 1, ndims < 0, a side < 1, product != n;
  *         EUNSUPPORTED for a side that is not a power of three with the latency-optimal or
@@ -141,7 +142,10 @@ int trivance_block_range(const trivance_plan_t* plan, int64_t elems, int collect
  * written once per pass). Latency-optimal: 2 S n elems w. Bandwidth-optimal: reduce-scatter step t
  * reads n elems w / 3^t and writes a third of that; all-gather step t reads n elems w / 3^(t+1)
  * and writes twice that; in total 3.5 w elems (n - 1) for divisible sizes (the exact sum over the
- * actual blocks is returned). w = 4 for both dtypes. Negative status on bad arguments.
+ * actual blocks is returned). Sides that are not powers of three: in every tree step each
+ * receiving rank reads its own partial and each sending child and writes once (reduce-scatter),
+ * or reads once and writes each child (all-gather). w = 4 for both dtypes. Negative status on bad
+ * arguments.
  */
 int64_t trivance_algorithmic_bytes(const trivance_plan_t* plan, int64_t elems, int dtype);
 
