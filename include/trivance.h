@@ -171,8 +171,10 @@ int64_t trivance_pass_bytes(const trivance_plan_t* plan, int64_t elems, int dtyp
  * bandwidth-optimal one leaves identical bits on every rank.
  *
  * Asynchronous: all passes are enqueued on `stream` and the call returns; execution errors
- * surface on stream synchronisation. No device memory is allocated and no host synchronisation
- * happens. n == 1 or elems == 0 is a valid no-op. Calls that overlap on the same buffers race.
+ * surface on stream synchronisation. No device memory is allocated, no memory is set and no host
+ * synchronisation happens, so the call can be captured into a HIP graph (replays reproduce it).
+ * n == 1 or elems == 0 is a valid no-op. Calls that overlap on the same buffers race; calls on
+ * different buffers may run concurrently on different streams.
  * Errors: EINVAL (NULL plan/buffers with elems > 0, n mismatch, elems < 0, bad dtype),
  * EUNSUPPORTED (a Bruck plan, sizes beyond 32-bit work-unit counts), EHIP (launch failure).
  */

@@ -371,3 +371,55 @@ def test_parity_largest_rings_sampled(n):
         assert_matches_oracle(got, np.ascontiguousarray(V[:, cols]), (n,), "B", col_seg=seg,
                               col_blk=blk, what=f"ring {n} {dtype}")
         del buf
+
+
+def test_two_streams_concurrently():
+    """Independent AllReduces enqueued on two streams (default priority) both match the oracle."""
+    import paper_2602_17254_amd as T
+
+    jobs = [((27,), "B", 64 * 27 * 3 + 4), ((3, 8), "B", 64 * 24 * 2 * 2 + 8), ((9,), "L", 4096)]
+    streams = [torch.cuda.Stream() for _ in jobs]
+    data = []
+    for (dims, variant, E), s in zip(jobs, streams):
+        n = int(np.prod(dims))
+        V = np.random.default_rng(E).standard_normal((n, E), dtype=np.float32)
+        buf = torch.from_numpy(V).cuda()
+        data.append((dims, variant, V, buf))
+    torch.cuda.synchronize()
+    for (dims, variant, V, buf), s in zip(data, streams):
+        _say(f"[streams] {dims} {variant}")
+        T.trivance_allreduce_emulated(buf, T.trivance_plan(dims, variant), stream=s)
+    for s in streams:
+        s.synchronize()
+    for dims, variant, V, buf in data:
+        assert_matches_oracle(buf.cpu().numpy(), V, dims, variant, what=f"stream {dims}")
+
+
+@pytest.mark.parametrize("dims,variant", [((27,), "B"), ((9,), "L"), ((3, 8), "B"), ((9, 9), "B")])
+def test_graph_capture_replays(dims, variant):
+    """The enqueued passes can be captured in a HIP graph: every replay (with eager refills and
+    synchronisation between replays) reproduces the eager result bit for bit."""
+    import paper_2602_17254_amd as T
+
+    n = int(np.prod(dims))
+    E = 64 * n * len(dims) * 2 + 4
+    plan = T.trivance_plan(dims, variant)
+    V = np.random.default_rng(n + E).standard_normal((n, E), dtype=np.float32)
+    src = torch.from_numpy(V).cuda()
+    buf = src.clone()
+    T.trivance_allreduce_emulated(buf, plan)
+    torch.cuda.synchronize()
+    eager = buf.clone()
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    buf.copy_(src)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=s):
+        T.trivance_allreduce_emulated(buf, plan)
+    for k in range(3):
+        _say(f"[graph] {dims} {variant} replay {k}")
+        buf.copy_(src)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(buf, eager), f"replay {k} differs from the eager result"
