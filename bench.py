@@ -96,11 +96,18 @@ def cpu_baseline(w, gpu_first_result_cols, cols, V_cols, seconds_target=15.0):
     sample_bytes = T.trivance_algorithmic_bytes(T.trivance_plan(w.dims, w.variant), w.elems) \
         * ncols / w.elems
     same = bool(np.array_equal(out, gpu_first_result_cols))
-    # the GPU's fp32 result on the sample against the fp64 sum: largest |error| / bound, where the
-    # bound is 4 S 2^-23 sum|v| (S = steps); below 1 means within the bound
-    S = T.trivance_plan(w.dims, w.variant).num_steps
-    err = np.abs(gpu_first_result_cols.astype(np.float64) - allreduce.fp64_sum(V_cols)[None, :])
-    margin = float((err / np.maximum(allreduce.fp32_error_bound(V_cols, S)[None, :], 1e-300)).max())
+    if V_cols.dtype == np.int32:
+        # integers: the exact column sums on every rank
+        exact = {"gpu_exact_int_sum_on_sample": bool(np.array_equal(
+            gpu_first_result_cols,
+            np.broadcast_to(allreduce.exact_int_sum(V_cols), gpu_first_result_cols.shape)))}
+    else:
+        # the GPU's fp32 result on the sample against the fp64 sum: largest |error| / bound, where
+        # the bound is 4 S 2^-23 sum|v| (S = steps); below 1 means within the bound
+        S = T.trivance_plan(w.dims, w.variant).num_steps
+        err = np.abs(gpu_first_result_cols.astype(np.float64) - allreduce.fp64_sum(V_cols)[None, :])
+        bound = np.maximum(allreduce.fp32_error_bound(V_cols, S)[None, :], 1e-300)
+        exact = {"gpu_fp64_bound_ratio_on_sample": round(float((err / bound).max()), 4)}
     return {
         "value": round(sample_bytes / dt / 1e9, 4),
         "unit": "GB/s",
@@ -110,7 +117,7 @@ def cpu_baseline(w, gpu_first_result_cols, cols, V_cols, seconds_target=15.0):
         "sample": f"{ncols} of {w.elems} columns x {w.n} ranks (all passes), {dt:.2f} s",
         "seconds": round(dt, 3),
         "matches_gpu_on_sample": same,
-        "gpu_fp64_bound_ratio_on_sample": round(margin, 4),
+        **exact,
     }
 
 
@@ -137,7 +144,7 @@ def _sample_for_baseline(w, budget_cols):
     return np.arange(start, start + budget_cols, dtype=np.int64)
 
 
-def run_workload(w, steps, warmup, with_cpu):
+def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
     import torch
 
     import paper_2602_17254_amd as T
@@ -145,18 +152,27 @@ def run_workload(w, steps, warmup, with_cpu):
     torch.cuda.set_device(0)
     plan = T.trivance_plan(w.dims, w.variant)
     P = plan.num_passes
-    alg_bytes = T.trivance_algorithmic_bytes(plan, w.elems)
-    pass_bytes = [T.trivance_pass_bytes(plan, w.elems, p) for p in range(P)]
+    code = {"f32": T.F32, "i32": T.I32}[dtype]
+    alg_bytes = T.trivance_algorithmic_bytes(plan, w.elems, code)
+    pass_bytes = [T.trivance_pass_bytes(plan, w.elems, p, code) for p in range(P)]
 
     # ---- inputs resident in HBM (untimed) ----
-    _say(f"[bench] {w.name}: preparing inputs ({w.n} x {w.elems} fp32)")
-    buf = torch.empty((w.n, w.elems), dtype=torch.float32, device="cuda")
-    if w.dist == "hash_uniform":
-        T.trivance_fill_hash_uniform(buf, w.seed)
-        V_host = None
-    else:
-        V_host = inputs.normal_f32(w.seed, w.n, w.elems)
+    _say(f"[bench] {w.name}: preparing inputs ({w.n} x {w.elems} {dtype})")
+    if dtype == "i32":
+        # the workload's int32 companion input: uniform integers in its stated range
+        if w.int_range is None:
+            raise ValueError(f"{w.name} has no int32 input")
+        buf = torch.empty((w.n, w.elems), dtype=torch.int32, device="cuda")
+        V_host = inputs.uniform_i32(w.int_seed, w.n, w.elems, *w.int_range)
         buf.copy_(torch.from_numpy(V_host))
+    else:
+        buf = torch.empty((w.n, w.elems), dtype=torch.float32, device="cuda")
+        if w.dist == "hash_uniform":
+            T.trivance_fill_hash_uniform(buf, w.seed)
+            V_host = None
+        else:
+            V_host = inputs.normal_f32(w.seed, w.n, w.elems)
+            buf.copy_(torch.from_numpy(V_host))
     torch.cuda.synchronize()
 
     # ---- first run: result kept for the CPU-baseline comparison ----
@@ -230,7 +246,8 @@ def run_workload(w, steps, warmup, with_cpu):
     dom_bytes = sum(pass_bytes[pb:pe]) / launches
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     src = os.path.join(ROOT, "paper_2602_17254_amd", "csrc", "executor.hip")
-    meas = MEASURED_TRAFFIC.get((w.name, names[dom]))
+    # counters were taken on the fp32 runs
+    meas = MEASURED_TRAFFIC.get((w.name, names[dom])) if dtype == "f32" else None
     traffic = None
     if meas and meas["src_sha"] == _src_sha(src):
         traffic = meas["bytes_per_launch"]
@@ -256,7 +273,7 @@ def run_workload(w, steps, warmup, with_cpu):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": dtype,
         "data": "synthetic",
         "config": {
             "workload": w.name,
@@ -267,7 +284,7 @@ def run_workload(w, steps, warmup, with_cpu):
             "rank_bytes": w.rank_bytes,
             "passes": P,
             "alg_bytes_per_step": alg_bytes,
-            "input": w.dist,
+            "input": w.dist if dtype == "f32" else f"uniform int32 {w.int_range}",
         },
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "step_ms_events": {"median": round(float(np.median(group_ms.sum(axis=1))), 4),
@@ -353,6 +370,8 @@ def main():
     ap.add_argument("--workload", default=inputs.HEADLINE, choices=sorted(inputs.WORKLOADS))
     ap.add_argument("--all", action="store_true", help="every named workload, one line each")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--dtype", default="f32", choices=["f32", "i32"],
+                    help="element type (i32 needs a workload with an int32 input)")
     ap.add_argument("--sweep", action="store_true",
                     help="8..128 MiB per rank for every topology/variant class")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -368,10 +387,15 @@ def main():
     if args.sweep:
         sweep(args.steps, args.warmup)
         return
-    names = list(inputs.WORKLOADS) if args.all else [args.workload]
-    for name in names:
+    if args.all:
+        # every workload in fp32, plus the int32 companion of those that define one
+        jobs = [(name, "f32") for name in inputs.WORKLOADS]
+        jobs += [(name, "i32") for name, w in inputs.WORKLOADS.items() if w.int_range is not None]
+    else:
+        jobs = [(args.workload, args.dtype)]
+    for name, dtype in jobs:
         line = run_workload(inputs.WORKLOADS[name], args.steps, args.warmup,
-                            with_cpu=not args.no_cpu_baseline)
+                            with_cpu=not args.no_cpu_baseline, dtype=dtype)
         print(json.dumps(line), flush=True)
 
 
