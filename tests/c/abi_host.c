@@ -1,0 +1,56 @@
+/* Host-only use of the C ABI from plain C (no GPU calls): plans, introspection, partition,
+ * byte accounting, the congestion length query and error codes. Exit status 0 on success. */
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "trivance.h"
+
+static int failures = 0;
+#define CHECK(cond)                                                        \
+    do {                                                                   \
+        if (!(cond)) {                                                     \
+            fprintf(stderr, "%s:%d: check failed: %s\n", __FILE__, __LINE__, #cond); \
+            ++failures;                                                    \
+        }                                                                  \
+    } while (0)
+
+int main(void) {
+    trivance_plan_t* p = NULL;
+    int dims[2] = {27, 27};
+    CHECK(trivance_plan(729, dims, 2, TRIVANCE_BANDWIDTH_OPT, &p) == TRIVANCE_OK && p != NULL);
+    CHECK(trivance_plan_num_steps(p) == 6);
+    CHECK(trivance_plan_num_passes(p) == 12);
+    int phase, step, dim, distance;
+    CHECK(trivance_plan_step(p, 0, 1, &phase, &step, &dim, &distance) == TRIVANCE_OK);
+    CHECK(phase == TRIVANCE_PHASE_REDUCE_SCATTER && step == 0 && dim == 1 && distance == 1);
+    CHECK(trivance_plan_step(p, 11, 0, &phase, &step, &dim, &distance) == TRIVANCE_OK);
+    CHECK(phase == TRIVANCE_PHASE_ALLGATHER && step == 0 && dim == 0 && distance == 1);
+    /* 3.5 w E (n - 1) for the bandwidth-optimal variant */
+    const int64_t E = 1048576;
+    CHECK(2 * trivance_algorithmic_bytes(p, E, TRIVANCE_F32) == 7 * 4 * E * 728);
+    int64_t b = -1, e = -1;
+    CHECK(trivance_block_range(p, E, 1, -1, &b, &e) == TRIVANCE_OK && b == E / 2 && e == E);
+    CHECK(trivance_block_range(p, E, 0, 0, &b, &e) == TRIVANCE_OK && b == 0 && e == 704);
+    CHECK(trivance_congestion(p, NULL, NULL, 0) == (int64_t)12 * 729 * 4);
+    CHECK(trivance_plan_step(p, 12, 0, &phase, &step, &dim, &distance) == TRIVANCE_EINVAL);
+    trivance_plan_destroy(p);
+
+    /* a ring whose size is not a power of three (Sec. 4.4): two steps at distances 1 and 3 */
+    trivance_plan_t* q = NULL;
+    CHECK(trivance_plan(8, NULL, 0, TRIVANCE_BANDWIDTH_OPT, &q) == TRIVANCE_OK);
+    CHECK(trivance_plan_num_steps(q) == 2);
+    CHECK(trivance_plan_step(q, 1, 0, NULL, NULL, NULL, &distance) == TRIVANCE_OK && distance == 3);
+    trivance_plan_destroy(q);
+
+    /* errors */
+    trivance_plan_t* r = NULL;
+    CHECK(trivance_plan(8, NULL, 0, TRIVANCE_LATENCY_OPT, &r) == TRIVANCE_EUNSUPPORTED && r == NULL);
+    CHECK(trivance_plan(80, dims, 2, TRIVANCE_LATENCY_OPT, &r) == TRIVANCE_EINVAL);
+    CHECK(trivance_allreduce_emulated(NULL, 9, 0, TRIVANCE_F32, NULL, NULL) == TRIVANCE_EINVAL);
+    CHECK(strcmp(trivance_strerror(TRIVANCE_ESIZE), "output buffer too small") == 0);
+    trivance_plan_destroy(NULL);
+
+    if (failures == 0) printf("abi_host ok\n");
+    return failures == 0 ? 0 : 1;
+}
