@@ -23,3 +23,25 @@ def test_c_program_uses_the_abi(tmp_path):
     res = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert res.returncode == 0, res.stdout + res.stderr
     assert "abi_host ok" in res.stdout
+
+
+@pytest.mark.gpu
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="gcc not found")
+def test_c_program_runs_allreduces_on_the_gpu(tmp_path):
+    """tests/c/abi_gpu.c: int32 AllReduces (ring, torus, ring of 8) and congestion from plain C,
+    with the HIP runtime API for device memory; exact sums and 3^k loads are checked in C."""
+    lib = os.path.join(PKG, "libtrivance.so")
+    if not os.path.exists(lib):
+        pytest.fail("libtrivance.so is not built")
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    exe = str(tmp_path / "abi_gpu")
+    subprocess.run(["gcc", "-std=c11", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+                    "-I", os.path.join(rocm, "include"), "-I", os.path.join(ROOT, "include"),
+                    os.path.join(ROOT, "tests", "c", "abi_gpu.c"),
+                    "-L", PKG, "-ltrivance", "-L", os.path.join(rocm, "lib"), "-lamdhip64",
+                    "-Wl,-rpath," + PKG, "-Wl,-rpath," + os.path.join(rocm, "lib"), "-o", exe],
+                   check=True)
+    print("[c-abi] running the C program on the GPU", flush=True)
+    res = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert "abi_gpu ok" in res.stdout
