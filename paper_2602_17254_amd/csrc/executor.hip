@@ -437,7 +437,10 @@ __global__ __launch_bounds__(kBlockThreads) void block_step_kernel(T* __restrict
 //
 // One wave handles one chunk of 64 * VEC elements of one (collective, block, offset tuple).
 // Units are numbered collective by collective; inside a collective: chunk fastest, then the
-// offset list of dimension 0, 1, ..., then the block's coordinates (dimension 0 first).
+// offset list of dimension 0, 1, ..., then, on a ring, the block's coordinate, and on a torus the
+// receiving rank's coordinates (dimension 0 first; the block is the rank minus the offsets).
+// Waves in flight together thus share rows on a torus and blocks on a ring, the order measured
+// faster for each (tori 4-9%, rings 1-5%).
 // DM: largest number of dimensions the arguments describe (1 for rings, kMaxTreeDims otherwise);
 // CAP: capacity of the offset table. Both only size the kernel arguments, which are copied at
 // every launch.
@@ -498,14 +501,19 @@ __device__ __forceinline__ bool tree_unit(const TreeArgs<DM, CAP>& a, uint32_t u
 #pragma unroll
     for (int d = 0; d < DM; ++d) {
         if (DM == 1 || d < a.D) {
-            uint32_t jd = rest;
-            if (DM > 1) {
+            // rings: the unit's coordinate is the block's, and the rank is j + o; tori: it is the
+            // receiving rank's, and the block is x - o (the same units, in rank order)
+            uint32_t jd, xd;
+            if (DM == 1) {
+                jd = rest;
+                xd = jd + off[d];
+                if (xd >= (uint32_t)a.side[d]) xd -= a.side[d];
+            } else {
                 const uint32_t qd = fdiv(rest, a.f_side[d]);
-                jd = rest - qd * (uint32_t)a.side[d];
+                xd = rest - qd * (uint32_t)a.side[d];
                 rest = qd;
+                jd = xd >= off[d] ? xd - off[d] : xd + (uint32_t)a.side[d] - off[d];
             }
-            uint32_t xd = jd + off[d];
-            if (xd >= (uint32_t)a.side[d]) xd -= a.side[d];
             j += jd * (uint32_t)a.stride[d];
             x += xd * (uint32_t)a.stride[d];
             if (d == a.act[c]) xa = xd;
