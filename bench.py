@@ -61,6 +61,17 @@ MEASURED_TRAFFIC = {
 }
 
 
+def phase_groups(phases):
+    """[begin, end, phase] of every maximal run of consecutive passes with the same phase."""
+    groups = []
+    for p, ph in enumerate(phases):
+        if groups and groups[-1][2] == ph:
+            groups[-1][1] = p + 1
+        else:
+            groups.append([p, p + 1, ph])
+    return groups
+
+
 def _is_pow3(v):
     while v % 3 == 0:
         v //= 3
@@ -198,13 +209,7 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
     # Passes of one phase run back to back with one kernel family (latency: every pass; reduce-
     # scatter; all-gather), so events at the phase boundaries give each family's average launch
     # duration (group time / launches) without a timing marker between every two kernels.
-    phases = [T.trivance_plan_step(plan, p)[0] for p in range(P)]
-    groups = []
-    for p, ph in enumerate(phases):
-        if groups and groups[-1][2] == ph:
-            groups[-1][1] = p + 1
-        else:
-            groups.append([p, p + 1, ph])
+    groups = phase_groups([T.trivance_plan_step(plan, p)[0] for p in range(P)])
     G = len(groups)
 
     # ---- timed region: K steps, events at the phase boundaries on the launch stream ----
