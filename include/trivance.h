@@ -204,7 +204,8 @@ int trivance_allreduce_emulated_steps(void* buffers, int n, int64_t elems, int d
  * swap).
  *
  * loads == NULL returns the required length (positive). ESIZE if loads_len is too small,
- * EUNSUPPORTED for a side above 6561. Allocates and frees a temporary device buffer.
+ * EUNSUPPORTED for a side above 6561 or 2^31 and more (pass, dimension, line) triples. Allocates
+ * and frees a temporary device buffer.
  */
 int64_t trivance_congestion(const trivance_plan_t* plan, const trivance_topology* topo,
                             int64_t* loads, int64_t loads_len);
@@ -221,6 +222,17 @@ int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topol
  * k = seed * 2^40 + r * elems + e + 1, mapped to (h >> 40) * 2^-23 - 1. Asynchronous on stream.
  */
 int trivance_fill_hash_uniform(void* buffers, int n, int64_t elems, uint64_t seed, void* stream);
+
+/*
+ * trivance_set_dispatch_limit -- the most work-items one kernel dispatch may hold (process-wide;
+ * default and maximum 2^31, minimum 1024). A dispatch carries its grid size as a 32-bit count of
+ * work-items, so every launch of this library whose grid is larger is issued as consecutive
+ * dispatches of whole workgroups on the same stream (the results do not depend on the split).
+ * A smaller limit only adds dispatches; it exists to exercise the split at small sizes. Set it
+ * while no call of this library is being enqueued. Returns the previous limit, or EINVAL for a
+ * value outside [1024, 2^31].
+ */
+int64_t trivance_set_dispatch_limit(int64_t work_items);
 
 /* Static description of a status code. */
 const char* trivance_strerror(int status);

@@ -71,6 +71,7 @@ def _lib():
         "trivance_congestion": (i64, [P, ctypes.POINTER(Topology), ctypes.POINTER(i64), i64]),
         "trivance_congestion_device": (ctypes.c_int, [P, ctypes.POINTER(Topology), P, i64, P]),
         "trivance_fill_hash_uniform": (ctypes.c_int, [P, ctypes.c_int, i64, ctypes.c_uint64, P]),
+        "trivance_set_dispatch_limit": (i64, [i64]),
         "trivance_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     }
     for name, (res, args) in sig.items():
@@ -88,7 +89,8 @@ def exported_symbols() -> list:
              "trivance_plan_num_passes", "trivance_plan_step", "trivance_block_range",
              "trivance_algorithmic_bytes", "trivance_pass_bytes", "trivance_allreduce_emulated",
              "trivance_allreduce_emulated_steps", "trivance_congestion",
-             "trivance_congestion_device", "trivance_fill_hash_uniform", "trivance_strerror"]
+             "trivance_congestion_device", "trivance_fill_hash_uniform",
+             "trivance_set_dispatch_limit", "trivance_strerror"]
     return [n for n in names if hasattr(lib, n)]
 
 
@@ -246,3 +248,9 @@ def trivance_fill_hash_uniform(buffers, seed: int, stream=None) -> None:
     _check(_lib().trivance_fill_hash_uniform(ctypes.c_void_p(buffers.data_ptr()),
                                              buffers.shape[0], buffers.shape[1], seed,
                                              _stream_ptr(stream)), "trivance_fill_hash_uniform")
+
+
+def trivance_set_dispatch_limit(work_items: int) -> int:
+    """Set the most work-items one kernel dispatch may hold (1024 .. 2^31); returns the previous
+    limit. Larger grids are issued as consecutive dispatches on the same stream."""
+    return _check(_lib().trivance_set_dispatch_limit(int(work_items)), "trivance_set_dispatch_limit")

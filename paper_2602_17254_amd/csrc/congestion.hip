@@ -39,6 +39,7 @@ struct CongArgs {
     int16_t distance[kMaxPasses][kMaxDims];  // per pass and collective (at most kMaxSide / 2)
     uint8_t dirs[kMaxPasses][kMaxDims];     // per pass and collective: bit 0 messages towards +, bit 1 towards -
     uint8_t act_dim[kMaxPasses][kMaxDims];
+    uint32_t wg_base;  // first workgroup of this dispatch (for_each_dispatch)
 };
 
 // Direction (+1 / -1) and hop count of a message over `offset` on a ring of `side` nodes.
@@ -83,7 +84,7 @@ __device__ __forceinline__ void add_range(int* diff, int* wraps, int s, int len,
 __global__ __launch_bounds__(64) void congestion_kernel(int64_t* __restrict__ loads, CongArgs a) {
     extern __shared__ int lds[];
     const int lane = threadIdx.x;
-    const uint32_t wg = blockIdx.x;
+    const uint32_t wg = a.wg_base + blockIdx.x;
     const int line = (int)(wg % (uint32_t)a.max_lines);
     const uint32_t rest = wg / (uint32_t)a.max_lines;
     const int dim = (int)(rest % (uint32_t)a.D);
@@ -207,11 +208,16 @@ int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topol
             }
         }
     }
-    const uint32_t grid = (uint32_t)((int64_t)P * plan->D * a.max_lines);
+    const int64_t grid = (int64_t)P * plan->D * a.max_lines;
+    if (grid >= ((int64_t)1 << 31)) return TRIVANCE_EUNSUPPORTED;
     const size_t lds = (size_t)(2 * max_side + 4) * sizeof(int);
-    hipLaunchKernelGGL(trivance::congestion_kernel, dim3(grid), dim3(64), lds,
-                       reinterpret_cast<hipStream_t>(stream), loads_dev, a);
-    return hipGetLastError() == hipSuccess ? TRIVANCE_OK : TRIVANCE_EHIP;
+    const bool ok = trivance::for_each_dispatch((uint64_t)grid, 64, [&](uint32_t first, uint32_t count) {
+        a.wg_base = first;
+        hipLaunchKernelGGL(trivance::congestion_kernel, dim3(count), dim3(64), lds,
+                           reinterpret_cast<hipStream_t>(stream), loads_dev, a);
+        return hipGetLastError() == hipSuccess;
+    });
+    return ok ? TRIVANCE_OK : TRIVANCE_EHIP;
 }
 
 int64_t trivance_congestion(const trivance_plan_t* plan, const trivance_topology* topo,

@@ -89,6 +89,7 @@ struct StepArgs {
     FastDiv f_side[kMaxDims];
     FastDiv f_mod[kMaxDims][kMaxDims];   // modulus[c][d]
     FastDiv f_nq[kMaxDims][kMaxDims];    // dims[d] / modulus[c][d]
+    uint32_t wg_base;              // first workgroup of this dispatch (for_each_dispatch)
 };
 
 template <typename T, int N>
@@ -168,7 +169,7 @@ template <typename T, int VEC, int VPT>
 __global__ __launch_bounds__(kBlockThreads) void latency_step_kernel(T* __restrict__ buf,
                                                                      StepArgs a) {
     using V = Vec<T, VEC>;
-    const uint32_t wg = blockIdx.x;
+    const uint32_t wg = a.wg_base + blockIdx.x;
     const uint32_t cb = wg % (uint32_t)a.colblocks;
     const uint32_t rest = wg / (uint32_t)a.colblocks;
     const int cyc = (int)(rest % (uint32_t)a.ncycles);
@@ -260,7 +261,7 @@ __global__ __launch_bounds__(64 * P) void latency_split_kernel(T* __restrict__ b
     constexpr int G = SUB / 3;
     __shared__ V halo[P][2][64];
 
-    const uint32_t wg = XCD ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x;
+    const uint32_t wg = a.wg_base + (XCD ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x);
     const uint32_t cb = wg % (uint32_t)a.colblocks;
     const uint32_t rest = wg / (uint32_t)a.colblocks;
     const int cyc = (int)(rest % (uint32_t)a.ncycles);
@@ -380,7 +381,7 @@ __global__ __launch_bounds__(kBlockThreads) void block_step_kernel(T* __restrict
     constexpr int kChunk = 64 * VEC * U;
     const int lane = threadIdx.x & 63;
     const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const uint32_t wg = XCD ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x;
+    const uint32_t wg = a.wg_base + (XCD ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x);
     const uint32_t unit = wg * (uint32_t)kWavesPerBlock + wave;
     if (unit >= a.total_units) return;
     Unit w;
@@ -462,6 +463,7 @@ struct TreeArgs {
     FastDiv f_cpb, f_n;
     FastDiv f_side[DM];
     FastDiv f_len[DM][DM];    // length of list (c, d)
+    uint32_t wg_base;         // first workgroup of this dispatch (for_each_dispatch)
     uint32_t tab[CAP];
 };
 static_assert(sizeof(TreeArgs<kMaxTreeDims, kMaxTab>) <= 4096,
@@ -557,7 +559,7 @@ __global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict_
     using V = Vec<T, VEC>;
     const int lane = threadIdx.x & 63;
     const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const uint32_t wg = xcd_contiguous(blockIdx.x, gridDim.x);
+    const uint32_t wg = a.wg_base + xcd_contiguous(blockIdx.x, gridDim.x);
     const uint32_t first = (wg * (uint32_t)kWavesPerBlock + wave) * (uint32_t)U;
     int64_t po[U], pl[U], pr[U];
     uint32_t fl[U];
@@ -591,6 +593,21 @@ __global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict_
 
 // ---------------------------------------------------------------------------------------------
 // Host side.
+
+// Enqueues `kernel` over `grid` workgroups of `threads` work-items as consecutive dispatches of
+// whole workgroups (for_each_dispatch), each with its first workgroup in the argument block.
+template <typename T, typename Args>
+hipError_t dispatch(void (*kernel)(T*, Args), uint64_t grid, int threads, hipStream_t stream,
+                    T* buf, Args a) {
+    hipError_t err = hipSuccess;
+    for_each_dispatch(grid, threads, [&](uint32_t first, uint32_t count) {
+        a.wg_base = first;
+        hipLaunchKernelGGL(kernel, dim3(count), dim3(threads), 0, stream, buf, a);
+        err = hipGetLastError();
+        return err == hipSuccess;
+    });
+    return err;
+}
 
 // Launch geometry of one pass.
 struct Launch {
@@ -677,10 +694,10 @@ inline void set_columns(StepArgs* a, Launch* L, int cols) {
 }
 
 template <typename T, int VEC, int SUB, int P, bool XCD = false>
-void launch_split(T* buf, StepArgs a, Launch L, hipStream_t stream) {
+hipError_t launch_split(T* buf, StepArgs a, Launch L, hipStream_t stream) {
     set_columns(&a, &L, 64);
-    hipLaunchKernelGGL((latency_split_kernel<T, VEC, SUB, P, 1, true, XCD>), dim3(L.grid),
-                       dim3(64 * P), 0, stream, buf, a);
+    return dispatch(latency_split_kernel<T, VEC, SUB, P, 1, true, XCD>, L.grid, 64 * P, stream,
+                    buf, a);
 }
 
 template <typename T, int VEC>
@@ -688,42 +705,33 @@ hipError_t launch_latency(T* buf, const StepArgs& a, const Launch& L, int len,
                           hipStream_t stream) {
     switch (len) {
         // rows per wavefront x wavefronts per workgroup, measured best on MI355X
-        case 3: launch_split<T, VEC, 3, 1>(buf, a, L, stream); break;
+        case 3: return launch_split<T, VEC, 3, 1>(buf, a, L, stream);
         case 9:
             // the XCD-contiguous workgroup order measured 4-13% faster for 9-row cycles on tori
             // of three or more dimensions, and 1.5-9% slower on rings
-            if (a.D >= 3)
-                launch_split<T, VEC, 3, 3, true>(buf, a, L, stream);
-            else
-                launch_split<T, VEC, 3, 3>(buf, a, L, stream);
-            break;
-        case 27: launch_split<T, VEC, 3, 9>(buf, a, L, stream); break;
-        case 81: launch_split<T, VEC, 9, 9>(buf, a, L, stream); break;
-        case 243: launch_split<T, VEC, 27, 9>(buf, a, L, stream); break;
+            if (a.D >= 3) return launch_split<T, VEC, 3, 3, true>(buf, a, L, stream);
+            return launch_split<T, VEC, 3, 3>(buf, a, L, stream);
+        case 27: return launch_split<T, VEC, 3, 9>(buf, a, L, stream);
+        case 81: return launch_split<T, VEC, 9, 9>(buf, a, L, stream);
+        case 243: return launch_split<T, VEC, 27, 9>(buf, a, L, stream);
         default: {
             StepArgs b = a;
             Launch M = L;
             set_columns(&b, &M, kBlockThreads);
-            hipLaunchKernelGGL((latency_step_kernel<T, VEC, 1>), dim3(M.grid),
-                               dim3(kBlockThreads), 0, stream, buf, b);
-            break;
+            return dispatch(latency_step_kernel<T, VEC, 1>, M.grid, kBlockThreads, stream, buf, b);
         }
     }
-    return hipGetLastError();
 }
 
 template <typename T, int VEC>
 hipError_t launch_block(T* buf, const StepArgs& a, const Launch& L, bool reduce,
                         hipStream_t stream) {
     if (L.U != 1) return hipErrorInvalidValue;
-    const dim3 grid(L.grid), block(kBlockThreads);
     if (reduce)
-        hipLaunchKernelGGL((block_step_kernel<T, VEC, 1, true, true, true>), grid, block, 0,
-                           stream, buf, a);
-    else
-        hipLaunchKernelGGL((block_step_kernel<T, VEC, 1, false, true, true>), grid, block, 0,
-                           stream, buf, a);
-    return hipGetLastError();
+        return dispatch(block_step_kernel<T, VEC, 1, true, true, true>, L.grid, kBlockThreads,
+                        stream, buf, a);
+    return dispatch(block_step_kernel<T, VEC, 1, false, true, true>, L.grid, kBlockThreads, stream,
+                    buf, a);
 }
 
 template <typename T, int VEC>
@@ -764,15 +772,15 @@ int run_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t 
 }
 
 template <typename T, int VEC, int U, int DM, int CAP>
-void launch_tree(T* buf, const TreeArgs<DM, CAP>& a, bool rs, int64_t total, hipStream_t stream) {
+hipError_t launch_tree(T* buf, const TreeArgs<DM, CAP>& a, bool rs, int64_t total,
+                       hipStream_t stream) {
     const int64_t waves = (total + U - 1) / U;
-    const dim3 grid((uint32_t)((waves + kWavesPerBlock - 1) / kWavesPerBlock));
+    const uint64_t grid = (uint64_t)((waves + kWavesPerBlock - 1) / kWavesPerBlock);
     if (rs)
-        hipLaunchKernelGGL((tree_step_kernel<T, VEC, U, true, DM, CAP>), grid, dim3(kBlockThreads),
-                           0, stream, buf, a);
-    else
-        hipLaunchKernelGGL((tree_step_kernel<T, VEC, U, false, DM, CAP>), grid,
-                           dim3(kBlockThreads), 0, stream, buf, a);
+        return dispatch(tree_step_kernel<T, VEC, U, true, DM, CAP>, grid, kBlockThreads, stream,
+                        buf, a);
+    return dispatch(tree_step_kernel<T, VEC, U, false, DM, CAP>, grid, kBlockThreads, stream, buf,
+                    a);
 }
 
 // Offset-table entries of pass `pi` (all collectives).
@@ -844,12 +852,13 @@ int run_tree_impl(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t s
         }
         if (total == 0) continue;
         const bool rs = ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER;
+        hipError_t err;
         switch (rs ? u_rs : u_ag) {
-            case 8: launch_tree<T, VEC, 8>(buf, a, rs, total, stream); break;
-            case 4: launch_tree<T, VEC, 4>(buf, a, rs, total, stream); break;
-            default: launch_tree<T, VEC, 1>(buf, a, rs, total, stream); break;
+            case 8: err = launch_tree<T, VEC, 8>(buf, a, rs, total, stream); break;
+            case 4: err = launch_tree<T, VEC, 4>(buf, a, rs, total, stream); break;
+            default: err = launch_tree<T, VEC, 1>(buf, a, rs, total, stream); break;
         }
-        if (hipGetLastError() != hipSuccess) return TRIVANCE_EHIP;
+        if (err != hipSuccess) return TRIVANCE_EHIP;
     }
     return TRIVANCE_OK;
 }

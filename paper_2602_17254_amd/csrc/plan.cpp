@@ -10,6 +10,7 @@
 // forwarded to peer p at step k are p + sum_{i>k} e_i 3^i; equivalently the blocks a rank keeps
 // after step k are those congruent to it modulo 3^(k+1). On a torus that congruence holds per
 // dimension, with the exponent counting the steps taken so far in that dimension.
+#include <atomic>
 #include <cmath>
 #include <cstdlib>
 #include <new>
@@ -174,9 +175,8 @@ int build_dim_tree(int n, trivance::DimTree* t) {
     for (long o = lo; o < lo + n; ++o) {
         if (o == 0) continue;
         const int side = fam[idx(o)];
-        long rel;
-        rel_in(o, side, &rel);
-        balanced_digits(rel, f, e);
+        long rel = 0;
+        if (!rel_in(o, side, &rel) || !balanced_digits(rel, f, e)) return TRIVANCE_EUNSUPPORTED;
         int k = f;
         int ek = side;
         long pw_k = 1;
@@ -305,9 +305,20 @@ int64_t max_block_granules(const trivance_plan_t* p, int64_t elems) {
     return best;
 }
 
+namespace {
+std::atomic<int64_t> g_dispatch_work_items{(int64_t)1 << 31};
+}  // namespace
+
+int64_t dispatch_work_items() { return g_dispatch_work_items.load(std::memory_order_relaxed); }
+
 }  // namespace trivance
 
 extern "C" {
+
+int64_t trivance_set_dispatch_limit(int64_t work_items) {
+    if (work_items < 1024 || work_items > ((int64_t)1 << 31)) return TRIVANCE_EINVAL;
+    return trivance::g_dispatch_work_items.exchange(work_items, std::memory_order_relaxed);
+}
 
 int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance_plan_t** out) {
     if (!out) return TRIVANCE_EINVAL;

@@ -1,6 +1,7 @@
 // Internal schedule representation shared by the host plan code and the HIP launchers.
 #pragma once
 
+#include <algorithm>
 #include <cstdint>
 #include <vector>
 
@@ -75,5 +76,21 @@ void block_bounds(const trivance_plan_t* p, int64_t elems, int c, int block, int
 
 // Largest number of granules in any block, over all segments.
 int64_t max_block_granules(const trivance_plan_t* p, int64_t elems);
+
+// Work-items of one kernel dispatch, at most (trivance_set_dispatch_limit; 2^31 by default).
+int64_t dispatch_work_items();
+
+// A dispatch packet holds its grid size as a 32-bit count of work-items, and a larger grid is not
+// rejected: it runs only part of the workgroups. Launches therefore go through this loop, which
+// splits a grid of `grid` workgroups of `threads` work-items into consecutive dispatches of at
+// most dispatch_work_items() work-items; one(first, count) enqueues workgroups
+// [first, first + count) and returns false on failure, which ends the loop.
+template <typename F>
+inline bool for_each_dispatch(uint64_t grid, int threads, F&& one) {
+    const uint64_t per = std::max<uint64_t>(1, (uint64_t)dispatch_work_items() / (uint64_t)threads);
+    for (uint64_t first = 0; first < grid; first += per)
+        if (!one((uint32_t)first, (uint32_t)std::min(per, grid - first))) return false;
+    return true;
+}
 
 }  // namespace trivance

@@ -49,6 +49,10 @@ int main(void) {
     CHECK(trivance_plan(80, dims, 2, TRIVANCE_LATENCY_OPT, &r) == TRIVANCE_EINVAL);
     CHECK(trivance_allreduce_emulated(NULL, 9, 0, TRIVANCE_F32, NULL, NULL) == TRIVANCE_EINVAL);
     CHECK(strcmp(trivance_strerror(TRIVANCE_ESIZE), "output buffer too small") == 0);
+    /* the dispatch limit: default 2^31, range [1024, 2^31], returns the previous value */
+    CHECK(trivance_set_dispatch_limit(1 << 20) == ((int64_t)1 << 31));
+    CHECK(trivance_set_dispatch_limit(100) == TRIVANCE_EINVAL);
+    CHECK(trivance_set_dispatch_limit((int64_t)1 << 31) == (1 << 20));
     trivance_plan_destroy(NULL);
 
     if (failures == 0) printf("abi_host ok\n");

@@ -107,6 +107,19 @@ def test_plan_errors():
     assert lib.trivance_strerror(-5) == b"output buffer too small"
 
 
+def test_dispatch_limit_range_and_previous_value():
+    prev = T.trivance_set_dispatch_limit(4096)
+    try:
+        assert prev == 2 ** 31
+        for bad in (0, -1, 1023, 2 ** 31 + 1):
+            with pytest.raises(T.TrivanceError):
+                T.trivance_set_dispatch_limit(bad)
+        assert T.trivance_set_dispatch_limit(1024) == 4096
+    finally:
+        T.trivance_set_dispatch_limit(prev)
+    assert T.trivance_set_dispatch_limit(2 ** 31) == 2 ** 31
+
+
 def test_congestion_length_query_and_size_check():
     """loads == NULL returns the required length; a short array is rejected before any GPU work."""
     lib = T.binding._lib()

@@ -1,5 +1,6 @@
 """The C ABI used from plain C: tests/c/abi_host.c is compiled as C11 against include/trivance.h,
-linked with libtrivance.so and run (host-only calls, no GPU needed)."""
+linked with libtrivance.so and run (host-only calls, no GPU needed); tests/c/dispatch_split.cpp
+checks the launch split of the host code with g++."""
 
 import os
 import shutil
@@ -23,6 +24,21 @@ def test_c_program_uses_the_abi(tmp_path):
     res = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert res.returncode == 0, res.stdout + res.stderr
     assert "abi_host ok" in res.stdout
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not found")
+def test_dispatch_split_covers_every_workgroup(tmp_path):
+    """tests/c/dispatch_split.cpp: the launch split keeps every dispatch within the work-item limit
+    and covers each workgroup exactly once, also for grids above 2^32 work-items (host only)."""
+    exe = str(tmp_path / "dispatch_split")
+    csrc = os.path.join(PKG, "csrc")
+    subprocess.run(["g++", "-std=c++17", "-O1", "-Wall", "-Wextra", "-Werror", "-I", csrc,
+                    "-I", os.path.join(ROOT, "include"),
+                    os.path.join(ROOT, "tests", "c", "dispatch_split.cpp"),
+                    os.path.join(csrc, "plan.cpp"), "-o", exe], check=True)
+    res = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert "dispatch_split ok" in res.stdout
 
 
 @pytest.mark.gpu
