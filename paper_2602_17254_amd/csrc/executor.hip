@@ -442,121 +442,195 @@ __global__ __launch_bounds__(kBlockThreads) void block_step_kernel(T* __restrict
 // receiving rank's coordinates (dimension 0 first; the block is the rank minus the offsets).
 // Waves in flight together thus share rows on a torus and blocks on a ring, the order measured
 // faster for each (tori 4-9%, rings 1-5%).
-// DM: largest number of dimensions the arguments describe (1 for rings, kMaxTreeDims otherwise);
-// CAP: capacity of the offset table. Both only size the kernel arguments, which are copied at
-// every launch.
+// DM: the number of dimensions (the decode is compiled for it); CAP: capacity of the offset table,
+// which sizes the kernel arguments, copied at every launch.
+//
+// The decode is wave-uniform (scalar unit). With blocks of a few granules the units are small
+// and the scalar unit, not HBM, bounds the step, so the host precomputes everything a unit needs
+// per collective, divisions take one 32-bit multiply-high, and the U consecutive units of a wave
+// are decoded incrementally: the next chunk of the same block, or the next offset of list 0
+// (same ranks on a torus, same block on a ring), reuse the previous unit's state.
+constexpr uint32_t kOffsetMask = 0x3FFFFFFFu;
+constexpr uint32_t kFlagBits = kFromLeft | kFromRight;
+
+// Per collective of one pass.
+template <int DM>
+struct TreeColl {
+    int64_t dE;           // elements from a rank's row to its neighbour's at +distance
+    int64_t spanE;        // elements spanned by the ring of the active dimension
+    int64_t g0, gc;       // first granule and number of granules of the segment
+    uint32_t begin;       // first unit of the collective
+    int act;              // active dimension
+    uint32_t dist;        // its distance
+    uint32_t side_act;    // its side
+    uint32_t len[DM];     // length of the offset list of dimension d
+    FastDiv32 f_len[DM];
+    uint16_t lstart[DM];  // first table entry of that list
+};
+
 template <int DM, int CAP>
 struct TreeArgs {
     int64_t elems;
-    int64_t seg_g0[DM];  // first granule of segment c
-    int64_t seg_gc[DM];  // granules of segment c
+    uint32_t total;       // units of the pass
     int n;
     int D;
-    int narrow;          // 1 if n * (granules of a segment + 1) < 2^31
-    int cpb;             // chunks per block (of the largest block)
+    int narrow;           // 1 if n * (granules of a segment + 1) < 2^31
+    int cpb;              // chunks per block (of the largest block)
     uint32_t unit_end[DM];  // collective c owns units [unit_end[c-1], unit_end[c])
-    int act[DM];         // active dimension of collective c
-    int dist[DM];        // its distance
-    int side[DM];
-    int stride[DM];
-    uint16_t lstart[DM][DM];  // first table entry of list (c, d)
-    FastDiv f_cpb, f_n;
-    FastDiv f_side[DM];
-    FastDiv f_len[DM][DM];    // length of list (c, d)
-    uint32_t wg_base;         // first workgroup of this dispatch (for_each_dispatch)
+    uint32_t side[DM];
+    uint32_t stride[DM];
+    FastDiv32 f_cpb, f_n;
+    FastDiv32 f_side[DM];
+    TreeColl<DM> coll[DM];
+    uint32_t wg_base;     // first workgroup of this dispatch (for_each_dispatch)
     uint32_t tab[CAP];
 };
 static_assert(sizeof(TreeArgs<kMaxTreeDims, kMaxTab>) <= 4096,
               "tree-step kernel arguments above 4 KiB");
 
-// Decodes work unit `unit` for this lane: element offsets of the own row and of the left and right
-// neighbours along the active dimension, and the receiver's flags. False if the lane has no
-// element in the unit (past the last unit or past the block's end).
+__device__ __forceinline__ uint32_t fdiv32(uint32_t x, FastDiv32 f) {
+    return __umulhi(x << 1, f.mul) >> f.shift;
+}
+
+// One decoded unit (wave-uniform) and the state its successors are derived from.
+struct TreeUnit {
+    int64_t row, rl, rr;  // element offsets of the own row and of its neighbours' rows
+    int64_t b, e;         // element range of the block
+    uint32_t chunk;
+    uint32_t fl;          // the active dimension's children (kFromLeft / kFromRight)
+    uint32_t i0;          // index in the offset list of dimension 0
+    uint32_t x0;          // torus: the rank's coordinate 0; ring: the block
+    uint32_t jrest;       // torus: the block minus its coordinate 0
+    int c;
+};
+
 template <int DM, int CAP>
-__device__ __forceinline__ bool tree_unit(const TreeArgs<DM, CAP>& a, uint32_t unit, int lane,
-                                          int chunk_elems, int vec, int64_t* own, int64_t* left,
-                                          int64_t* right, uint32_t* flags) {
-    if (unit >= a.unit_end[DM == 1 ? 0 : a.D - 1]) return false;
+__device__ __forceinline__ void tree_rows(const TreeArgs<DM, CAP>& a, const TreeColl<DM>& k,
+                                          uint32_t x, uint32_t xa, TreeUnit* w) {
+    w->row = (int64_t)x * a.elems;
+    w->rl = w->row - k.dE + (xa < k.dist ? k.spanE : 0);
+    w->rr = w->row + k.dE - (xa + k.dist >= k.side_act ? k.spanE : 0);
+}
+
+template <int DM, int CAP>
+__device__ __forceinline__ void tree_block(const TreeArgs<DM, CAP>& a, const TreeColl<DM>& k,
+                                           uint32_t j, TreeUnit* w) {
+    int64_t gb, ge;
+    if (a.narrow) {
+        const uint32_t p = j * (uint32_t)k.gc;
+        gb = k.g0 + fdiv32(p, a.f_n);
+        ge = k.g0 + fdiv32(p + (uint32_t)k.gc, a.f_n);
+    } else {
+        gb = k.g0 + (int64_t)j * k.gc / a.n;
+        ge = k.g0 + (int64_t)(j + 1) * k.gc / a.n;
+    }
+    w->b = imin64(gb * kGranule, a.elems);
+    w->e = imin64(ge * kGranule, a.elems);
+}
+
+// Full decode of `unit`; false past the pass's last unit.
+template <int DM, int CAP>
+__device__ __forceinline__ bool tree_decode(const TreeArgs<DM, CAP>& a, uint32_t unit,
+                                            TreeUnit* w) {
+    if (unit >= a.total) return false;
     int c = 0;
 #pragma unroll
     for (int i = 0; i < DM - 1; ++i)
-        if (i + 1 < a.D && unit >= a.unit_end[i]) c = i + 1;
-    uint32_t rest = unit - (c > 0 ? a.unit_end[c > 0 ? c - 1 : 0] : 0u);
-    const uint32_t q = fdiv(rest, a.f_cpb);
-    const uint32_t chunk = rest - q * (uint32_t)a.cpb;
+        if (unit >= a.unit_end[i]) c = i + 1;
+    const TreeColl<DM>& k = a.coll[c];
+    w->c = c;
+    uint32_t rest = unit - k.begin;
+    uint32_t q = fdiv32(rest, a.f_cpb);
+    w->chunk = rest - q * (uint32_t)a.cpb;
     rest = q;
-    uint32_t off[DM];
-    uint32_t fl = 0;
+    uint32_t e[DM];
 #pragma unroll
     for (int d = 0; d < DM; ++d) {
-        off[d] = 0;
-        if (DM == 1 || d < a.D) {
-            const uint32_t qd = fdiv(rest, a.f_len[c][d]);
-            const uint32_t i = rest - qd * a.f_len[c][d].d;
-            rest = qd;
-            const uint32_t e = a.tab[a.lstart[c][d] + i];
-            off[d] = e & 0x3FFFFFFFu;
-            if (d == a.act[c]) fl = e & (kFromLeft | kFromRight);
-        }
+        q = fdiv32(rest, k.f_len[d]);
+        const uint32_t i = rest - q * k.len[d];
+        rest = q;
+        if (d == 0) w->i0 = i;
+        e[d] = a.tab[k.lstart[d] + i];
     }
-    uint32_t j = 0, x = 0, xa = 0;
+    if (DM == 1) {
+        // ring: the block is j = rest, its rank j + offset
+        const uint32_t off = e[0] & kOffsetMask;
+        uint32_t x = rest + off;
+        if (x >= a.side[0]) x -= a.side[0];
+        w->x0 = rest;
+        w->fl = e[0] & kFlagBits;
+        tree_rows(a, k, x, x, w);
+        tree_block(a, k, rest, w);
+        return true;
+    }
+    // torus: rest is the rank (dimension 0 fastest); the block is the rank minus the offsets
+    const uint32_t x = rest;
+    uint32_t j = 0, xa = 0, fl = 0, jd0 = 0;
 #pragma unroll
     for (int d = 0; d < DM; ++d) {
-        if (DM == 1 || d < a.D) {
-            // rings: the unit's coordinate is the block's, and the rank is j + o; tori: it is the
-            // receiving rank's, and the block is x - o (the same units, in rank order)
-            uint32_t jd, xd;
-            if (DM == 1) {
-                jd = rest;
-                xd = jd + off[d];
-                if (xd >= (uint32_t)a.side[d]) xd -= a.side[d];
-            } else {
-                const uint32_t qd = fdiv(rest, a.f_side[d]);
-                xd = rest - qd * (uint32_t)a.side[d];
-                rest = qd;
-                jd = xd >= off[d] ? xd - off[d] : xd + (uint32_t)a.side[d] - off[d];
-            }
-            j += jd * (uint32_t)a.stride[d];
-            x += xd * (uint32_t)a.stride[d];
-            if (d == a.act[c]) xa = xd;
+        uint32_t xd = rest;
+        if (d + 1 < DM) {
+            q = fdiv32(rest, a.f_side[d]);
+            xd = rest - q * a.side[d];
+            rest = q;
+        }
+        const uint32_t off = e[d] & kOffsetMask;
+        const uint32_t jd = xd >= off ? xd - off : xd + a.side[d] - off;
+        j += jd * a.stride[d];
+        if (d == k.act) {
+            xa = xd;
+            fl = e[d] & kFlagBits;
+        }
+        if (d == 0) {
+            w->x0 = xd;
+            jd0 = jd;
         }
     }
-    const int ad = DM == 1 ? 0 : a.act[c];
-    const uint32_t sa = (uint32_t)a.stride[ad];
-    const uint32_t dist = (uint32_t)a.dist[c];
-    const uint32_t span = (uint32_t)a.side[ad] * sa;
-    const uint32_t xl = xa >= dist ? x - dist * sa : x + span - dist * sa;
-    const uint32_t xr = xa + dist < (uint32_t)a.side[ad] ? x + dist * sa : x + dist * sa - span;
-
-    const int64_t g0 = a.seg_g0[c];
-    const int64_t gc = a.seg_gc[c];
-    int64_t gb, ge;
-    if (a.narrow) {
-        gb = g0 + fdiv(j * (uint32_t)gc, a.f_n);
-        ge = g0 + fdiv((j + 1) * (uint32_t)gc, a.f_n);
-    } else {
-        gb = g0 + (int64_t)j * gc / a.n;
-        ge = g0 + (int64_t)(j + 1) * gc / a.n;
-    }
-    const int64_t E = a.elems;
-    const int64_t b = imin64(gb * kGranule, E);
-    const int64_t e = imin64(ge * kGranule, E);
-    const int64_t idx = b + (int64_t)chunk * chunk_elems + (int64_t)lane * vec;
-    if (idx >= e) return false;
-    *own = (int64_t)x * E + idx;
-    *left = (int64_t)xl * E + idx;
-    *right = (int64_t)xr * E + idx;
-    *flags = fl;
+    w->fl = fl;
+    w->jrest = j - jd0;
+    tree_rows(a, k, x, xa, w);
+    tree_block(a, k, j, w);
     return true;
 }
 
-// One unit per wave (decoded with wave-uniform arithmetic); a wave takes U consecutive units and
-// issues all their loads before the first store, which keeps more bytes in flight per wave when
-// blocks fill only part of a chunk.
+// Moves a decoded unit to `unit` = its successor; full decode when more than the chunk and the
+// offset of list 0 change.
+template <int DM, int CAP>
+__device__ __forceinline__ bool tree_next(const TreeArgs<DM, CAP>& a, uint32_t unit,
+                                          TreeUnit* w) {
+    if (w->chunk + 1 < (uint32_t)a.cpb) {
+        ++w->chunk;
+        return true;
+    }
+    const TreeColl<DM>& k = a.coll[w->c];
+    if (w->i0 + 1 < k.len[0]) {
+        w->chunk = 0;
+        ++w->i0;
+        const uint32_t e0 = a.tab[k.lstart[0] + w->i0];
+        const uint32_t off = e0 & kOffsetMask;
+        if (DM == 1) {
+            uint32_t x = w->x0 + off;
+            if (x >= a.side[0]) x -= a.side[0];
+            w->fl = e0 & kFlagBits;
+            tree_rows(a, k, x, x, w);
+        } else {
+            const uint32_t xd = w->x0;
+            const uint32_t jd = xd >= off ? xd - off : xd + a.side[0] - off;
+            if (k.act == 0) w->fl = e0 & kFlagBits;
+            tree_block(a, k, w->jrest + jd, w);
+        }
+        return true;
+    }
+    return tree_decode(a, unit, w);
+}
+
+// A wave takes U consecutive units and issues all their loads before the first store, which
+// keeps more bytes in flight per wave when blocks fill only part of a chunk.
 template <typename T, int VEC, int U, bool REDUCE, int DM, int CAP>
 __global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict__ buf,
                                                                    TreeArgs<DM, CAP> a) {
     using V = Vec<T, VEC>;
+    constexpr int kChunk = 64 * VEC;
     const int lane = threadIdx.x & 63;
     const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t wg = a.wg_base + xcd_contiguous(blockIdx.x, gridDim.x);
@@ -565,9 +639,17 @@ __global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict_
     uint32_t fl[U];
     bool ok[U];
     V vo[U], vl[U], vr[U];
+    TreeUnit w;
+    bool live = tree_decode(a, first, &w);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        ok[u] = tree_unit(a, first + u, lane, 64 * VEC, VEC, &po[u], &pl[u], &pr[u], &fl[u]);
+        if (u > 0 && live) live = tree_next(a, first + u, &w);
+        const int64_t idx = w.b + (int64_t)w.chunk * kChunk + (int64_t)lane * VEC;
+        ok[u] = live && idx < w.e;
+        po[u] = w.row + idx;
+        pl[u] = w.rl + idx;
+        pr[u] = w.rr + idx;
+        fl[u] = w.fl;
         if (ok[u]) {
             vo[u] = ld<T, VEC, true>(buf + po[u]);
             if (REDUCE) {
@@ -802,60 +884,68 @@ int run_tree_impl(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t s
     a.elems = elems;
     a.n = p->n;
     a.D = p->D;
-    int64_t max_gc = 0;
+    int64_t max_gc = 0, seg_g0[kMaxTreeDims] = {}, seg_gc[kMaxTreeDims] = {};
     const int64_t G = (elems + kGranule - 1) / kGranule;
     for (int c = 0; c < p->D; ++c) {
-        a.seg_g0[c] = (int64_t)c * G / p->D;
-        a.seg_gc[c] = (int64_t)(c + 1) * G / p->D - a.seg_g0[c];
-        max_gc = std::max(max_gc, a.seg_gc[c]);
+        seg_g0[c] = (int64_t)c * G / p->D;
+        seg_gc[c] = (int64_t)(c + 1) * G / p->D - seg_g0[c];
+        max_gc = std::max(max_gc, seg_gc[c]);
     }
     a.narrow = (int64_t)p->n * (max_gc + 1) < ((int64_t)1 << 31) ? 1 : 0;
-    a.f_n = make_fastdiv((uint32_t)p->n);
+    a.f_n = make_fastdiv32((uint32_t)p->n);
     for (int d = 0; d < p->D; ++d) {
-        a.side[d] = p->dims[d];
-        a.stride[d] = p->strides[d];
-        a.f_side[d] = make_fastdiv((uint32_t)p->dims[d]);
+        a.side[d] = (uint32_t)p->dims[d];
+        a.stride[d] = (uint32_t)p->strides[d];
+        a.f_side[d] = make_fastdiv32((uint32_t)p->dims[d]);
     }
     const int64_t max_blk = max_block_granules(p, elems) * kGranule;
     const int64_t chunk = 64 * VEC;
     a.cpb = (int)std::max<int64_t>(1, (max_blk + chunk - 1) / chunk);
-    a.f_cpb = make_fastdiv((uint32_t)a.cpb);
-    // Units per wave, measured on MI355X over rings and 2- to 4-dimensional tori: the
-    // reduce-scatter takes four when the blocks fill less than 80% of their chunks on average
-    // (blocks of a few granules, e.g. 16 x 16 x 16 ranks at 8 MiB) and one otherwise; the
-    // all-gather (one load per unit) takes eight on tori of three or more dimensions whose blocks
-    // average under 4096 elements, and otherwise follows the reduce-scatter rule.
+    a.f_cpb = make_fastdiv32((uint32_t)a.cpb);
+    // Units per wave, measured on MI355X over rings and 2- to 4-dimensional tori. When blocks
+    // fill less than 80% of their chunks on average (blocks of a few granules, e.g. 16 x 16 x 16
+    // ranks at 8 and 16 MiB, 32 x 32 at 1 MiB) the all-gather (one load per unit) takes eight,
+    // and the reduce-scatter two on rings and 2D tori; everything else takes one.
     const double fill = (double)elems / ((double)p->D * p->n * a.cpb * chunk);
-    const int u_rs = fill < 0.8 ? 4 : 1;
-    const int u_ag = (p->D >= 3 && elems < (int64_t)4096 * p->D * p->n) ? 8 : u_rs;
+    const int u_rs = fill < 0.8 && p->D <= 2 ? 2 : 1;
+    const int u_ag = fill < 0.8 ? 8 : 1;
     for (int pi = pb; pi < pe; ++pi) {
         const Pass& ps = p->passes[pi];
         int used = 0;
         int64_t total = 0;
         for (int c = 0; c < p->D; ++c) {
+            TreeColl<DM>& k = a.coll[c];
             const int ad = ps.dim[c];
-            a.act[c] = ad;
-            a.dist[c] = ps.distance[c];
+            k.act = ad;
+            k.dist = (uint32_t)ps.distance[c];
+            k.side_act = (uint32_t)p->dims[ad];
+            k.dE = (int64_t)ps.distance[c] * p->strides[ad] * elems;
+            k.spanE = (int64_t)p->dims[ad] * p->strides[ad] * elems;
+            k.g0 = seg_g0[c];
+            k.gc = seg_gc[c];
+            k.begin = (uint32_t)total;
             int64_t units = (int64_t)p->n * a.cpb;
             for (int d = 0; d < p->D; ++d) {
                 const std::vector<uint32_t>& list =
                     d == ad ? p->trees[d].recv[ps.dim_step[c]] : p->trees[d].alive[ps.taken[c][d]];
                 if (used + (int)list.size() > CAP) return TRIVANCE_EUNSUPPORTED;
-                a.lstart[c][d] = (uint16_t)used;
+                k.lstart[d] = (uint16_t)used;
                 for (uint32_t v : list) a.tab[used++] = v;
-                a.f_len[c][d] = make_fastdiv((uint32_t)std::max<size_t>(1, list.size()));
+                k.len[d] = (uint32_t)list.size();
+                k.f_len[d] = make_fastdiv32((uint32_t)std::max<size_t>(1, list.size()));
                 units *= (int64_t)list.size();
             }
             total += units;
             if (total >= ((int64_t)1 << 31) - 4096) return TRIVANCE_EUNSUPPORTED;
             a.unit_end[c] = (uint32_t)total;
         }
+        a.total = (uint32_t)total;
         if (total == 0) continue;
         const bool rs = ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER;
         hipError_t err;
         switch (rs ? u_rs : u_ag) {
             case 8: err = launch_tree<T, VEC, 8>(buf, a, rs, total, stream); break;
-            case 4: err = launch_tree<T, VEC, 4>(buf, a, rs, total, stream); break;
+            case 2: err = launch_tree<T, VEC, 2>(buf, a, rs, total, stream); break;
             default: err = launch_tree<T, VEC, 1>(buf, a, rs, total, stream); break;
         }
         if (err != hipSuccess) return TRIVANCE_EHIP;
@@ -863,8 +953,8 @@ int run_tree_impl(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t s
     return TRIVANCE_OK;
 }
 
-// Rings take the one-dimensional decode; plans whose passes need at most 64 table entries take
-// the short argument block.
+// The decode is compiled per number of dimensions (1 to 4); plans whose passes need at most 64
+// table entries take the short argument block.
 template <typename T, int VEC>
 int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
                     int pe) {
@@ -875,9 +965,15 @@ int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t
     if (p->D == 1)
         return small ? run_tree_impl<T, VEC, 1, 64>(buf, elems, p, stream, pb, pe)
                      : run_tree_impl<T, VEC, 1, kMaxTab>(buf, elems, p, stream, pb, pe);
-    if (p->D > kMaxTreeDims) return TRIVANCE_EUNSUPPORTED;
-    return small ? run_tree_impl<T, VEC, kMaxTreeDims, 64>(buf, elems, p, stream, pb, pe)
-                 : run_tree_impl<T, VEC, kMaxTreeDims, kMaxTab>(buf, elems, p, stream, pb, pe);
+    switch (p->D) {
+        case 2: return small ? run_tree_impl<T, VEC, 2, 64>(buf, elems, p, stream, pb, pe)
+                             : run_tree_impl<T, VEC, 2, kMaxTab>(buf, elems, p, stream, pb, pe);
+        case 3: return small ? run_tree_impl<T, VEC, 3, 64>(buf, elems, p, stream, pb, pe)
+                             : run_tree_impl<T, VEC, 3, kMaxTab>(buf, elems, p, stream, pb, pe);
+        case 4: return small ? run_tree_impl<T, VEC, 4, 64>(buf, elems, p, stream, pb, pe)
+                             : run_tree_impl<T, VEC, 4, kMaxTab>(buf, elems, p, stream, pb, pe);
+        default: return TRIVANCE_EUNSUPPORTED;
+    }
 }
 
 template <typename T>

@@ -77,6 +77,27 @@ void block_bounds(const trivance_plan_t* p, int64_t elems, int c, int block, int
 // Largest number of granules in any block, over all segments.
 int64_t max_block_granules(const trivance_plan_t* p, int64_t elems);
 
+// Division by an invariant d >= 1 of dividends below 2^31 with one 32-bit multiply-high:
+// x / d == mulhi(2 x, mul) >> shift, shift = ceil(log2 d), mul = floor(2^(31 + shift) / d) + 1
+// (Granlund and Montgomery, "Division by invariant integers using multiplication", PLDI 1994,
+// with N = 31; mul < 2^32 because d > 2^(shift - 1)). The doubled dividend turns their shift by
+// 31 + shift into the high word's shift by `shift`.
+struct FastDiv32 {
+    uint32_t mul;
+    uint32_t shift;
+};
+
+inline FastDiv32 make_fastdiv32(uint32_t d) {
+    uint32_t l = 0;
+    while (((uint64_t)1 << l) < d) ++l;
+    return FastDiv32{(uint32_t)((((uint64_t)1 << (31 + l)) / d) + 1), l};
+}
+
+// Host form of the device division (for tests): x < 2^31.
+inline uint32_t fastdiv32_host(uint32_t x, FastDiv32 f) {
+    return (uint32_t)((((uint64_t)(x << 1) * f.mul) >> 32) >> f.shift);
+}
+
 // Work-items of one kernel dispatch, at most (trivance_set_dispatch_limit; 2^31 by default).
 int64_t dispatch_work_items();
 

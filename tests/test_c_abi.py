@@ -1,6 +1,6 @@
 """The C ABI used from plain C: tests/c/abi_host.c is compiled as C11 against include/trivance.h,
 linked with libtrivance.so and run (host-only calls, no GPU needed); tests/c/dispatch_split.cpp
-checks the launch split of the host code with g++."""
+and tests/c/fastdiv.cpp check the launch split and the invariant division with g++."""
 
 import os
 import shutil
@@ -39,6 +39,21 @@ def test_dispatch_split_covers_every_workgroup(tmp_path):
     res = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert res.returncode == 0, res.stdout + res.stderr
     assert "dispatch_split ok" in res.stdout
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not found")
+def test_invariant_division_is_exact(tmp_path):
+    """tests/c/fastdiv.cpp: the 32-bit multiply-high division of the tree-step decode equals the
+    hardware division for every divisor up to 2^16 at the extreme dividends and for 8 million
+    seeded random (dividend < 2^31, divisor) pairs (host only)."""
+    exe = str(tmp_path / "fastdiv")
+    csrc = os.path.join(PKG, "csrc")
+    subprocess.run(["g++", "-std=c++17", "-O2", "-Wall", "-Wextra", "-Werror", "-I", csrc,
+                    "-I", os.path.join(ROOT, "include"), os.path.join(ROOT, "tests", "c", "fastdiv.cpp"),
+                    "-o", exe], check=True)
+    res = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert "fastdiv ok" in res.stdout
 
 
 @pytest.mark.gpu

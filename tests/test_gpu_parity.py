@@ -234,7 +234,8 @@ NONPOW3 = [(2, 100), (4, 64 * 4 * 3 + 4), (5, 999), (7, 64 * 7 * 5 + 12), (8, 64
            (10, 3001), (16, 64 * 16 * 2 + 8), (20, 64 * 20 * 3 + 4), (32, 64 * 32 + 20),
            (50, 7777), (64, 64 * 64 + 4), (100, 64 * 100 + 36), (250, 64 * 250 + 4),
            (728, 64 * 728 + 8),
-           # blocks filling whole 256-element chunks: one unit per wave (the others take four)
+           # blocks filling whole 256-element chunks: one unit per wave (the others above take two
+           # in the reduce-scatter and eight in the all-gather)
            (8, 8 * 256 * 3 + 4), (20, 20 * 256 * 2)]
 
 
@@ -271,11 +272,13 @@ NONPOW3_TORI = [((4, 4), 64 * 16 * 2 * 3 + 4), ((2, 3), 101), ((8, 8), 64 * 64 *
                 ((4, 4, 4), 64 * 64 * 3 + 20), ((2, 3, 4), 999), ((2, 2, 2, 2), 64 * 16 * 4 + 4),
                 ((10, 3, 3), 64 * 90 * 3 + 4), ((16, 16), 64 * 256 * 2 + 36), ((4, 4), 5),
                 ((8, 8), 0),
-                # blocks filling whole 256-element chunks: one unit per wave
+                # blocks filling whole 256-element chunks: one unit per wave in both phases (the
+                # partly filled ones above take two (2D) or one (3D, 4D) in the reduce-scatter and
+                # eight in the all-gather)
                 ((4, 4), 2 * 16 * 256 * 2), ((2, 3, 4), 3 * 24 * 256 + 12),
-                # three dimensions with blocks of at least 4096 elements: one unit per wave in
-                # the all-gather (eight below that)
-                ((2, 2, 2), 3 * 8 * 4096 + 192)]
+                ((2, 2, 2), 3 * 8 * 4096 + 192), ((2, 2, 2, 2), 4 * 16 * 256 * 2),
+                # more than 64 offset-table entries per pass on 2D and 4D tori (the long table)
+                ((20, 20), 64 * 400 * 2 // 3 + 4), ((5, 5, 5, 5), 4001)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "i32"])
