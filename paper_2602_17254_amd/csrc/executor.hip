@@ -41,27 +41,21 @@ namespace {
 constexpr int kBlockThreads = 256;
 constexpr int kWavesPerBlock = kBlockThreads / 64;
 
-// Division by a per-pass constant d via a precomputed multiplier: for 0 <= x < 2^31,
-// x / d == (x * mul) >> shift with shift = 31 + ceil(log2 d), mul = floor(2^shift / d) + 1
-// (Granlund and Montgomery, "Division by invariant integers using multiplication", PLDI 1994).
+// Division by a per-pass constant d of dividends below 2^31 (FastDiv32 in plan.h: one 32-bit
+// multiply-high and a shift), with the divisor kept for remainders.
 struct FastDiv {
-    uint64_t mul;
+    uint32_t mul;
     uint32_t shift;
     uint32_t d;
 };
 
 inline FastDiv make_fastdiv(uint32_t d) {
-    uint32_t l = 0;
-    while (((uint64_t)1 << l) < d) ++l;
-    FastDiv f;
-    f.d = d;
-    f.shift = 31 + l;
-    f.mul = (((uint64_t)1 << f.shift) / d) + 1;
-    return f;
+    const FastDiv32 f = make_fastdiv32(d);
+    return FastDiv{f.mul, f.shift, d};
 }
 
 __device__ __forceinline__ uint32_t fdiv(uint32_t x, const FastDiv& f) {
-    return (uint32_t)(((uint64_t)x * f.mul) >> f.shift);
+    return __umulhi(x << 1, f.mul) >> f.shift;
 }
 
 struct StepArgs {
