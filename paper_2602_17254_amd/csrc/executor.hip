@@ -459,7 +459,7 @@ struct TreeColl {
     uint32_t side_act;    // its side
     uint32_t len[DM];     // length of the offset list of dimension d
     FastDiv32 f_len[DM];
-    uint16_t lstart[DM];  // first table entry of that list
+    uint32_t lstart[DM];  // first table entry of that list
 };
 
 template <int DM, int CAP>
@@ -923,7 +923,7 @@ int run_tree_impl(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t s
                 const std::vector<uint32_t>& list =
                     d == ad ? p->trees[d].recv[ps.dim_step[c]] : p->trees[d].alive[ps.taken[c][d]];
                 if (used + (int)list.size() > CAP) return TRIVANCE_EUNSUPPORTED;
-                k.lstart[d] = (uint16_t)used;
+                k.lstart[d] = (uint32_t)used;
                 for (uint32_t v : list) a.tab[used++] = v;
                 k.len[d] = (uint32_t)list.size();
                 k.f_len[d] = make_fastdiv32((uint32_t)std::max<size_t>(1, list.size()));
