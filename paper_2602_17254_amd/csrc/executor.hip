@@ -790,6 +790,8 @@ hipError_t launch_latency(T* buf, const StepArgs& a, const Launch& L, int len,
         case 27: return launch_split<T, VEC, 3, 9>(buf, a, L, stream);
         case 81: return launch_split<T, VEC, 9, 9>(buf, a, L, stream);
         case 243: return launch_split<T, VEC, 27, 9>(buf, a, L, stream);
+        // 81 rows per wavefront keep the register window in registers (72 VGPRs); 243 would spill
+        case 729: return launch_split<T, VEC, 81, 9>(buf, a, L, stream);
         default: {
             StepArgs b = a;
             Launch M = L;

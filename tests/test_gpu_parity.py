@@ -39,7 +39,7 @@ SHAPES = [
     ((9,), 0), ((9,), 7), ((9,), 64), ((9,), 1024), ((9,), 64 * 9 * 3 + 20), ((9,), 12345),
     ((27,), 64 * 27 * 4 + 4), ((27,), 5003),
     ((81,), 64 * 81 * 2 + 8), ((81,), 20001),
-    ((243,), 64 * 243 * 2 + 4),
+    ((243,), 64 * 243 * 2 + 4), ((729,), 64 * 729 + 8),
     ((3, 3), 5), ((3, 3), 64 * 9 * 4 + 12), ((3, 3), 3333),
     ((9, 9), 64 * 81 * 3 + 4), ((9, 9), 7777),
     ((3, 3, 3), 64 * 27 * 3 + 16), ((3, 3, 3), 999),
