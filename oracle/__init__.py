@@ -20,6 +20,9 @@ congestion  hop-by-hop link-load walk (cost model of Sec. 2.1) and the transmiss
 nonpow3     rings and tori whose sides are not all powers of three (Sec. 4.4): the final-step
             distance, the reduction tree of every side, a mailbox emulation of the bandwidth-
             optimal variant and a column-by-column gather form of it, and their link loads.
+placement   an optional block placement (not the default partition): block j at the position
+            spelled by its base-3 digits in the order the schedule fixes them, which makes every
+            kept set and message contiguous.
 
 Parity status: every function here is pinned by a `-m "not gpu"` test against values the paper
 prints, closed forms or brute force, except the floating-point summation order of the joint
@@ -28,6 +31,9 @@ pinned only through the invariants listed in tests/test_oracle_allreduce.py. The
 of sides that are not powers of three are a reading too (nonpow3): integer sums, forwarding
 counts, the 7-node figure, the final-step congestion and agreement with the ordinary schedule on
 powers of three pin them; the fp32 association they produce beyond that is parity unpinned.
+The optional placement is pinned by the digit reversal it reduces to on a ring, by the contiguity
+of the kept sets Algorithm 1 yields, and by the per-block equality with the latency-optimal
+result at the block's owner.
 """
 
-from . import schedule, partition, allreduce, congestion  # noqa: F401
+from . import schedule, partition, allreduce, congestion, placement  # noqa: F401
