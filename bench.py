@@ -90,10 +90,13 @@ def _say(msg):
 def cpu_baseline(w, gpu_first_result_cols, cols, V_cols, seconds_target=15.0):
     """Time the CPU oracle (as it stands, single-threaded numpy) on a column sample of the same
     workload, and compare its result with the GPU's first AllReduce on those columns."""
-    from oracle import allreduce, partition
+    from oracle import allreduce, partition, placement
 
     D = len(w.dims)
-    seg, blk = partition.column_labels(w.elems, D, w.n, cols)
+    if w.placement == "schedule":
+        seg, blk = placement.column_labels(w.elems, w.dims, cols)
+    else:
+        seg, blk = partition.column_labels(w.elems, D, w.n, cols)
     t0 = time.perf_counter()
     if w.variant == "L":
         out = allreduce.latency_optimal(V_cols, w.dims, col_seg=seg)
@@ -104,7 +107,8 @@ def cpu_baseline(w, gpu_first_result_cols, cols, V_cols, seconds_target=15.0):
     import paper_2602_17254_amd as T
 
     ncols = len(cols)
-    sample_bytes = T.trivance_algorithmic_bytes(T.trivance_plan(w.dims, w.variant), w.elems) \
+    sample_bytes = T.trivance_algorithmic_bytes(T.trivance_plan(w.dims, w.variant, w.placement),
+                                                w.elems) \
         * ncols / w.elems
     same = bool(np.array_equal(out, gpu_first_result_cols))
     if V_cols.dtype == np.int32:
@@ -161,7 +165,7 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
     import paper_2602_17254_amd as T
 
     torch.cuda.set_device(0)
-    plan = T.trivance_plan(w.dims, w.variant)
+    plan = T.trivance_plan(w.dims, w.variant, w.placement)
     P = plan.num_passes
     code = {"f32": T.F32, "i32": T.I32}[dtype]
     alg_bytes = T.trivance_algorithmic_bytes(plan, w.elems, code)
@@ -284,6 +288,7 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
             "workload": w.name,
             "topology": "x".join(map(str, w.dims)),
             "variant": {"L": "latency-optimal", "B": "bandwidth-optimal"}[w.variant],
+            "block_placement": "schedule digits" if w.placement == "schedule" else "natural",
             "n_ranks": w.n,
             "elems_per_rank": w.elems,
             "rank_bytes": w.rank_bytes,

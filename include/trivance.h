@@ -102,6 +102,25 @@ typedef enum {
  */
 int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance_plan_t** out);
 
+/* Plan option (trivance_plan_ex): message-contiguous block placement. */
+#define TRIVANCE_PLACE_BY_SCHEDULE 1u
+
+/*
+ * trivance_plan_ex -- trivance_plan with options.
+ *   flags  0, or TRIVANCE_PLACE_BY_SCHEDULE: block j of every segment lies at the granule range of
+ *          position pos_c(j) instead of the j-th one (see trivance_block_range). pos_c(j) spells
+ *          the base-3 digits of block j's coordinates in the order collective c's steps fix them
+ *          (step t fixes digit t div D of dimension (c + t) mod D), most significant first. The
+ *          blocks a rank keeps after each reduce-scatter step (Sec. 4.3 closed form) and every
+ *          message are then one contiguous range of positions. Power-of-three sides of equal
+ *          length, bandwidth-optimal variant only (EUNSUPPORTED otherwise). The option changes
+ *          which elements share a block, hence an element's fp32 summation tree; int32 results
+ *          are the same exact sums.
+ * Errors: those of trivance_plan, and EINVAL for unknown flag bits.
+ */
+int trivance_plan_ex(int n, const int* torus_dims, int ndims, int variant, unsigned flags,
+                     trivance_plan_t** out);
+
 /* Release a plan (NULL is ignored). */
 void trivance_plan_destroy(trivance_plan_t* plan);
 
@@ -130,6 +149,8 @@ int trivance_plan_step(const trivance_plan_t* plan, int pass, int collective, in
  * rule used here: 64-element granules, G = ceil(elems / 64); segment c holds granules
  * [floor(c G / D), floor((c+1) G / D)); block j of a G_c-granule segment holds its granules
  * [floor(j G_c / n), floor((j+1) G_c / n)); bounds are clipped at elems. Blocks may be empty.
+ * Plans made with TRIVANCE_PLACE_BY_SCHEDULE place block j at the range of position pos_c(j)
+ * (trivance_plan_ex) instead of the j-th range.
  * block == -1 returns the whole segment. Block j is owned (finished) by rank j.
  * EINVAL for a NULL output, elems < 0, or an index out of range.
  */

@@ -24,6 +24,8 @@ PHASE_LATENCY, PHASE_REDUCE_SCATTER, PHASE_ALLGATHER = 0, 1, 2
 MAX_DIMS = 8
 
 _VARIANTS = {"L": LATENCY_OPT, "B": BANDWIDTH_OPT, "BRUCK": BRUCK_REF}
+PLACE_BY_SCHEDULE = 1  # TRIVANCE_PLACE_BY_SCHEDULE
+_PLACEMENTS = {"natural": 0, "schedule": PLACE_BY_SCHEDULE}
 _ROUTING = {"scheduled": ROUTE_SCHEDULED, "shortest": ROUTE_SHORTEST}
 
 
@@ -56,6 +58,8 @@ def _lib():
     sig = {
         "trivance_plan": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ctypes.c_int), ctypes.c_int,
                                          ctypes.c_int, ctypes.POINTER(P)]),
+        "trivance_plan_ex": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ctypes.c_int), ctypes.c_int,
+                                            ctypes.c_int, ctypes.c_uint, ctypes.POINTER(P)]),
         "trivance_plan_destroy": (None, [P]),
         "trivance_plan_num_steps": (ctypes.c_int, [P]),
         "trivance_plan_num_passes": (ctypes.c_int, [P]),
@@ -85,7 +89,7 @@ def _lib():
 def exported_symbols() -> list:
     """Names the binding resolves (all of include/trivance.h)."""
     lib = ctypes.CDLL(LIB_PATH)
-    names = ["trivance_plan", "trivance_plan_destroy", "trivance_plan_num_steps",
+    names = ["trivance_plan", "trivance_plan_ex", "trivance_plan_destroy", "trivance_plan_num_steps",
              "trivance_plan_num_passes", "trivance_plan_step", "trivance_block_range",
              "trivance_algorithmic_bytes", "trivance_pass_bytes", "trivance_allreduce_emulated",
              "trivance_allreduce_emulated_steps", "trivance_congestion",
@@ -103,10 +107,11 @@ def _check(rc: int, what: str) -> int:
 class Plan:
     """Owns a trivance_plan_t handle."""
 
-    def __init__(self, handle, dims, variant):
+    def __init__(self, handle, dims, variant, placement="natural"):
         self._h = handle
         self.dims = tuple(dims)
         self.variant = variant
+        self.placement = placement
         self.n = int(np.prod(self.dims))
         self.D = len(self.dims)
 
@@ -128,15 +133,16 @@ class Plan:
             self._h = None
 
 
-def trivance_plan(dims, variant="L") -> Plan:
-    """Build a plan for a ring (dims=(n,)) or torus; variant 'L', 'B' or 'BRUCK'."""
+def trivance_plan(dims, variant="L", placement="natural") -> Plan:
+    """Build a plan for a ring (dims=(n,)) or torus; variant 'L', 'B' or 'BRUCK'; placement
+    'natural' (block j at the j-th granule range) or 'schedule' (TRIVANCE_PLACE_BY_SCHEDULE)."""
     dims = tuple(int(d) for d in dims)
     arr = (ctypes.c_int * len(dims))(*dims)
     h = ctypes.c_void_p()
     n = int(np.prod(dims)) if dims else 0
-    _check(_lib().trivance_plan(n, arr, len(dims), _VARIANTS[variant], ctypes.byref(h)),
-           "trivance_plan")
-    return Plan(h, dims, variant)
+    _check(_lib().trivance_plan_ex(n, arr, len(dims), _VARIANTS[variant], _PLACEMENTS[placement],
+                                   ctypes.byref(h)), "trivance_plan_ex")
+    return Plan(h, dims, variant, placement)
 
 
 def trivance_plan_step(plan: Plan, pass_index: int, collective: int = 0) -> tuple:

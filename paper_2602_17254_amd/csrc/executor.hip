@@ -84,6 +84,10 @@ struct StepArgs {
     FastDiv f_mod[kMaxDims][kMaxDims];   // modulus[c][d]
     FastDiv f_nq[kMaxDims][kMaxDims];    // dims[d] / modulus[c][d]
     uint32_t wg_base;              // first workgroup of this dispatch (for_each_dispatch)
+    // block steps of plans placed by schedule digits (TRIVANCE_PLACE_BY_SCHEDULE)
+    int placed;
+    int S;                                 // steps per phase
+    uint8_t pdig[kMaxDims][kMaxDims];     // digits of dimension d that collective c has fixed
 };
 
 template <typename T, int N>
@@ -311,6 +315,12 @@ __global__ __launch_bounds__(64 * P) void latency_split_kernel(T* __restrict__ b
 
 // ---------------------------------------------------------------------------------------------
 // Decode of a block-step work unit (all values wave-uniform).
+
+// 3^e for the digit weights of placed plans (n < 2^31, so e <= 19).
+__constant__ uint32_t kPow3[20] = {1u,        3u,         9u,         27u,        81u,
+                                   243u,      729u,       2187u,      6561u,      19683u,
+                                   59049u,    177147u,    531441u,    1594323u,   4782969u,
+                                   14348907u, 43046721u,  129140163u, 387420489u, 1162261467u};
 struct Unit {
     int64_t begin, end;  // element range of this unit's chunk (begin < end when active)
     int rank, left, right;
@@ -326,21 +336,46 @@ __device__ __forceinline__ bool decode_unit(const StepArgs& a, uint32_t unit, in
     uint32_t q = pair - r * (uint32_t)a.kept;
     const int act = a.act_dim[c];
 
+    // j: the block (default partition) or its position (placed plans)
     uint32_t j = 0, rr = r, r_act = 0;
+    if (a.placed) {
+        // the centre keeps the blocks that agree with it in the digits fixed so far, which sit
+        // at one run of positions: the centre's own fixed digits, most significant first (digit
+        // k of dimension d was fixed at step k D + ((d - c) mod D)), then q
+        const uint32_t q0 = q;
 #pragma unroll
-    for (int d = 0; d < kMaxDims; ++d) {
-        if (d < a.D) {
-            const uint32_t rr_next = fdiv(rr, a.f_side[d]);
-            const uint32_t rd = rr - rr_next * (uint32_t)a.dims[d];
-            rr = rr_next;
-            const FastDiv& fk = a.f_mod[c][d];
-            const FastDiv& fq = a.f_nq[c][d];
-            const uint32_t q_next = fdiv(q, fq);
-            const uint32_t qd = q - q_next * fq.d;
-            q = q_next;
-            const uint32_t rd_mod = rd - fdiv(rd, fk) * fk.d;
-            j += (rd_mod + fk.d * qd) * (uint32_t)a.strides[d];
-            if (d == act) r_act = rd;
+        for (int d = 0; d < kMaxDims; ++d) {
+            if (d < a.D) {
+                const uint32_t rr_next = fdiv(rr, a.f_side[d]);
+                uint32_t x = rr - rr_next * (uint32_t)a.dims[d];
+                rr = rr_next;
+                if (d == act) r_act = x;
+                const int delta = d >= (int)c ? d - (int)c : d + a.D - (int)c;
+                int e = a.S - 1 - delta;
+                for (int k = 0; k < (int)a.pdig[c][d]; ++k, e -= a.D) {
+                    const uint32_t x3 = __umulhi(x, 0xAAAAAAABu) >> 1;  // x / 3
+                    j += (x - 3u * x3) * kPow3[e];
+                    x = x3;
+                }
+            }
+        }
+        j += q0;
+    } else {
+#pragma unroll
+        for (int d = 0; d < kMaxDims; ++d) {
+            if (d < a.D) {
+                const uint32_t rr_next = fdiv(rr, a.f_side[d]);
+                const uint32_t rd = rr - rr_next * (uint32_t)a.dims[d];
+                rr = rr_next;
+                const FastDiv& fk = a.f_mod[c][d];
+                const FastDiv& fq = a.f_nq[c][d];
+                const uint32_t q_next = fdiv(q, fq);
+                const uint32_t qd = q - q_next * fq.d;
+                q = q_next;
+                const uint32_t rd_mod = rd - fdiv(rd, fk) * fk.d;
+                j += (rd_mod + fk.d * qd) * (uint32_t)a.strides[d];
+                if (d == act) r_act = rd;
+            }
         }
     }
     const int side = a.dims[act];
@@ -709,6 +744,8 @@ inline int base_args(const trivance_plan_t* p, int64_t elems, StepArgs* out, int
     for (int c = 0; c < p->D; ++c) max_gc = std::max<int64_t>(max_gc, a.seg_g[c + 1] - a.seg_g[c]);
     a.narrow = (int64_t)p->n * (max_gc + 1) < ((int64_t)1 << 31) ? 1 : 0;
     a.f_n = make_fastdiv((uint32_t)p->n);
+    a.placed = p->placed ? 1 : 0;
+    a.S = p->S;
     for (int d = 0; d < kMaxDims; ++d) a.f_side[d] = make_fastdiv((uint32_t)a.dims[d]);
     *max_blk = max_block_granules(p, elems) * kGranule;
     if (*max_blk >= ((int64_t)1 << 31)) return TRIVANCE_EUNSUPPORTED;
@@ -728,6 +765,9 @@ inline int pass_args(const trivance_plan_t* p, const Pass& ps, int64_t max_blk, 
             a->modulus[c][d] = m;
             a->f_mod[c][d] = make_fastdiv((uint32_t)m);
             a->f_nq[c][d] = make_fastdiv((uint32_t)(a->dims[d] / m));
+            int digits = 0;
+            for (int v = m; v > 1; v /= 3) ++digits;
+            a->pdig[c][d] = (uint8_t)digits;
         }
     }
     a->kept = (int)ps.kept_per_rank;

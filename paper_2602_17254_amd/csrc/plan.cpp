@@ -279,8 +279,27 @@ int build_tree_plan(trivance_plan_t* p) {
 
 namespace trivance {
 
+int placed_position(const trivance_plan_t* p, int c, int block) {
+    // equal sides: step t of collective c works on dimension (c + t) mod D and fixes the next
+    // digit (digit t div D) of that coordinate
+    int coord[kMaxDims];
+    int rest = block;
+    for (int d = 0; d < p->D; ++d) {
+        coord[d] = rest % p->dims[d];
+        rest /= p->dims[d];
+    }
+    int pos = 0;
+    for (int t = 0; t < p->S; ++t) {
+        const int d = (c + t) % p->D;
+        pos = 3 * pos + coord[d] % 3;
+        coord[d] /= 3;
+    }
+    return pos;
+}
+
 void block_bounds(const trivance_plan_t* p, int64_t elems, int c, int block, int64_t* begin,
                   int64_t* end) {
+    if (block >= 0 && p->placed) block = placed_position(p, c, block);
     const int64_t G = (elems + kGranule - 1) / kGranule;
     const int64_t g0 = (int64_t)c * G / p->D;
     const int64_t g1 = (int64_t)(c + 1) * G / p->D;
@@ -321,8 +340,14 @@ int64_t trivance_set_dispatch_limit(int64_t work_items) {
 }
 
 int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance_plan_t** out) {
+    return trivance_plan_ex(n, torus_dims, ndims, variant, 0u, out);
+}
+
+int trivance_plan_ex(int n, const int* torus_dims, int ndims, int variant, unsigned flags,
+                     trivance_plan_t** out) {
     if (!out) return TRIVANCE_EINVAL;
     *out = nullptr;
+    if (flags & ~TRIVANCE_PLACE_BY_SCHEDULE) return TRIVANCE_EINVAL;
     if (n < 1 || ndims < 0) return TRIVANCE_EINVAL;
     if (variant < TRIVANCE_LATENCY_OPT || variant > TRIVANCE_BRUCK_REF) return TRIVANCE_EINVAL;
     int dims[kMaxDims] = {};
@@ -343,6 +368,11 @@ int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance
     }
     bool pow3 = true;
     for (int d = 0; d < D; ++d) pow3 = pow3 && log3_exact(dims[d]) >= 0;
+    if (flags & TRIVANCE_PLACE_BY_SCHEDULE) {
+        bool equal = true;
+        for (int d = 1; d < D; ++d) equal = equal && dims[d] == dims[0];
+        if (!pow3 || !equal || variant != TRIVANCE_BANDWIDTH_OPT) return TRIVANCE_EUNSUPPORTED;
+    }
     // Sec. 4.4 (sides that are not powers of three): bandwidth-optimal variant only
     if (!pow3) {
         if (variant != TRIVANCE_BANDWIDTH_OPT || D > trivance::kMaxTreeDims)
@@ -412,6 +442,7 @@ int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance
         return TRIVANCE_ENOMEM;
     }
     delete rot;
+    p->placed = (flags & TRIVANCE_PLACE_BY_SCHEDULE) != 0;
     *out = p;
     return TRIVANCE_OK;
 }

@@ -66,6 +66,9 @@ struct trivance_plan {
     // while its offset from j, in every dimension, has not yet been forwarded.
     bool tree = false;
     std::vector<trivance::DimTree> trees;
+    // TRIVANCE_PLACE_BY_SCHEDULE (equal power-of-three sides, bandwidth-optimal): block j of
+    // segment c lies at position trivance::placed_position(p, c, j).
+    bool placed = false;
 };
 
 namespace trivance {
@@ -73,6 +76,10 @@ namespace trivance {
 // Element range [begin, end) of block `block` (or the whole segment for block < 0) of segment c.
 void block_bounds(const trivance_plan_t* p, int64_t elems, int c, int block, int64_t* begin,
                   int64_t* end);
+
+// Position of block `block` of segment c under TRIVANCE_PLACE_BY_SCHEDULE: the base-3 digits of
+// its coordinates in the order collective c's steps fix them, most significant first.
+int placed_position(const trivance_plan_t* p, int c, int block);
 
 // Largest number of granules in any block, over all segments.
 int64_t max_block_granules(const trivance_plan_t* p, int64_t elems);

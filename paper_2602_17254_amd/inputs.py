@@ -63,6 +63,8 @@ class Workload:
     dist      'normal' (N(0,1) fp32 from numpy) or 'hash_uniform' (U(-1,1), generated on device)
     seed      seed of the fp32 input
     int_range inclusive int32 range of the bit-exact integer companion run, or None
+    placement 'natural' (block j at the j-th granule range) or 'schedule' (blocks placed by the
+              digits the schedule fixes, TRIVANCE_PLACE_BY_SCHEDULE)
     """
 
     name: str
@@ -74,6 +76,7 @@ class Workload:
     int_range: tuple | None = None
     congestion: bool = False
     tags: tuple = field(default_factory=tuple)
+    placement: str = "natural"
 
     @property
     def n(self) -> int:
@@ -110,6 +113,14 @@ WORKLOADS = {
                  ("nonpower3",)),
         Workload("torus16x16x16_B_8MiB", (16, 16, 16), "B", 2_097_152, "hash_uniform", 9, None,
                  False, ("nonpower3",)),
+        # the power-of-three bandwidth-optimal workloads with message-contiguous block placement
+        # (same inputs as their default-partition counterparts)
+        Workload("ring243_Bp_32MiB", (243,), "B", 8_388_608, "normal", 2, (-(2 ** 20), 2 ** 20),
+                 False, ("placed",), "schedule"),
+        Workload("torus27x27_Bp_4MiB", (27, 27), "B", 1_048_576, "normal", 3, None, False,
+                 ("placed",), "schedule"),
+        Workload("torus9x9x9_Bp_128MiB", (9, 9, 9), "B", 33_554_432, "hash_uniform", 4, None,
+                 False, ("placed",), "schedule"),
     ]
 }
 

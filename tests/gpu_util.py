@@ -9,12 +9,12 @@ from oracle import allreduce, nonpow3, partition, schedule
 VARIANT_NAMES = {"L": "latency-optimal", "B": "bandwidth-optimal"}
 
 
-def run_hip(V: np.ndarray, dims, variant: str) -> np.ndarray:
+def run_hip(V: np.ndarray, dims, variant: str, placement: str = "natural") -> np.ndarray:
     import torch
 
     import paper_2602_17254_amd as T
 
-    plan = T.trivance_plan(dims, variant)
+    plan = T.trivance_plan(dims, variant, placement)
     buf = torch.from_numpy(np.ascontiguousarray(V)).cuda()
     T.trivance_allreduce_emulated(buf, plan)
     torch.cuda.synchronize()
@@ -63,7 +63,7 @@ def assert_matches_oracle(got: np.ndarray, V: np.ndarray, dims, variant: str, co
 
 
 def sample_columns(E: int, D: int, n: int, variant: str, seed: int, per_block: int = 2,
-                   max_blocks: int | None = None):
+                   max_blocks: int | None = None, dims=None, placement: str = "natural"):
     """Deterministic column sample of a large run: for every (segment, block) its first and last
     element and `per_block` seeded random ones (variant B), or segment ends plus random columns
     (variant L). With max_blocks, only that many seeded blocks per segment (always including the
@@ -85,5 +85,15 @@ def sample_columns(E: int, D: int, n: int, variant: str, seed: int, per_block: i
             if e > b:
                 cols += [b, e - 1] + rng.integers(b, e, 2000).tolist()
     cols = np.unique(np.array(cols, dtype=np.int64))
-    seg, blk = partition.column_labels(E, D, n, cols)
+    if placement == "schedule":
+        # the same granule ranges, now labelled with the block placed there
+        seg, blk = placement_labels(E, dims, cols)
+    else:
+        seg, blk = partition.column_labels(E, D, n, cols)
     return cols, seg, blk
+
+
+def placement_labels(E: int, dims, cols=None):
+    from oracle import placement
+
+    return placement.column_labels(E, dims, cols)

@@ -107,6 +107,33 @@ def test_plan_errors():
     assert lib.trivance_strerror(-5) == b"output buffer too small"
 
 
+@pytest.mark.parametrize("dims,E", [((9,), 64 * 9 * 3 + 20), ((243,), 8 * 2 ** 20), ((27, 27), 1_048_576),
+                                    ((9, 9, 9), 12345), ((3, 3, 3, 3), 5000), ((1,), 100)])
+def test_placed_block_range_matches_oracle_placement(dims, E):
+    from oracle import placement
+
+    p = T.trivance_plan(dims, "B", placement="schedule")
+    nat = partition.block_bounds(E, p.D, p.n)
+    pos = placement.positions(dims)
+    for c in range(p.D):
+        for j in range(p.n):
+            assert T.trivance_block_range(p, E, c, j) == nat[c][pos[c][j]]
+        assert T.trivance_block_range(p, E, c, -1) == partition.segment_bounds(E, p.D)[c]
+
+
+def test_placement_is_rejected_where_it_does_not_apply():
+    lib = T.binding._lib()
+    for dims, variant in [((8,), "B"), ((9, 27), "B"), ((9,), "L"), ((9,), "BRUCK"), ((4, 4), "B")]:
+        with pytest.raises(T.TrivanceError) as e:
+            T.trivance_plan(dims, variant, placement="schedule")
+        assert e.value.status == -2
+    h = ctypes.c_void_p()
+    arr = (ctypes.c_int * 1)(9)
+    assert lib.trivance_plan_ex(9, arr, 1, 1, 2, ctypes.byref(h)) == -1
+    assert lib.trivance_plan_ex(9, arr, 1, 1, 0, ctypes.byref(h)) == 0
+    lib.trivance_plan_destroy(h)
+
+
 def test_dispatch_limit_range_and_previous_value():
     prev = T.trivance_set_dispatch_limit(4096)
     try:

@@ -86,6 +86,20 @@ def test_split_dispatches_match_oracle(dims, variant, E, dtype):
         np.testing.assert_array_equal(got, np.broadcast_to(allreduce.exact_int_sum(V), got.shape))
 
 
+@pytest.mark.parametrize("dims,E", [((243,), 64 * 243 + 4), ((9, 9, 9), 64 * 729 + 100)])
+def test_split_dispatches_placed(dims, E):
+    """Message-contiguous placement with one to sixteen workgroups per dispatch."""
+    from gpu_util import placement_labels
+
+    n = int(np.prod(dims))
+    V = np.random.default_rng(n + E).integers(-(2 ** 31), 2 ** 31 - 1, size=(n, E), dtype=np.int32)
+    _say(f"[split placed] dims={dims} E={E} limit=1024")
+    with _Limit(1024):
+        got = run_hip(V, dims, "B", placement="schedule")
+    seg, blk = placement_labels(E, dims)
+    assert_matches_oracle(got, V, dims, "B", col_seg=seg, col_blk=blk, what=f"split placed {dims}")
+
+
 @pytest.mark.parametrize("dims,variant", [((27, 27), "B"), ((81,), "L"), ((8,), "B"),
                                           ((4, 4, 4), "B"), ((9,), "BRUCK")])
 def test_split_congestion_matches_oracle(dims, variant):

@@ -426,3 +426,57 @@ def test_graph_capture_replays(dims, variant):
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(buf, eager), f"replay {k} differs from the eager result"
+
+
+# Message-contiguous block placement (TRIVANCE_PLACE_BY_SCHEDULE): bandwidth-optimal, equal
+# power-of-three sides; against the oracle with the placed block labels
+PLACED = [((3,), 64 * 3 * 5 + 4), ((9,), 7), ((9,), 64 * 9 * 3 + 20), ((27,), 5003),
+          ((81,), 64 * 81 * 2 + 8), ((243,), 64 * 243 * 2 + 4), ((729,), 64 * 729 + 8),
+          ((3, 3), 3333), ((9, 9), 64 * 81 * 3 + 4), ((27, 27), 64 * 729 + 36),
+          ((3, 3, 3), 64 * 27 * 3 + 16), ((9, 9, 9), 64 * 729 * 2 + 100),
+          ((3, 3, 3, 3), 64 * 81 * 4 + 12), ((1,), 5), ((9,), 0)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "i32"])
+@pytest.mark.parametrize("dims,E", PLACED, ids=[_ids(p) for p in PLACED])
+def test_parity_placed(dims, E, dtype):
+    from gpu_util import placement_labels
+
+    n = int(np.prod(dims))
+    rng = np.random.default_rng(31 * n + E)
+    _say(f"[placed] dims={dims} E={E} dtype={dtype}")
+    if dtype == "f32":
+        V = rng.standard_normal((n, E), dtype=np.float32)
+    else:
+        V = rng.integers(-(2 ** 31), 2 ** 31 - 1, size=(n, E), dtype=np.int32)
+    got = run_hip(V, dims, "B", placement="schedule")
+    seg, blk = placement_labels(E, dims)
+    assert_matches_oracle(got, V, dims, "B", col_seg=seg, col_blk=blk,
+                          what=f"placed {dims} E={E} {dtype}")
+    if dtype == "i32":
+        np.testing.assert_array_equal(got, np.broadcast_to(allreduce.exact_int_sum(V), got.shape))
+
+
+@pytest.mark.parametrize("dims", [(27,), (9, 9), (3, 3, 3)])
+def test_placed_step_hook_reduce_scatter_then_resume(dims):
+    """Placed plans: the state after the reduce-scatter passes equals the oracle's, and resuming
+    with the all-gather passes completes the AllReduce."""
+    import paper_2602_17254_amd as T
+    from gpu_util import placement_labels
+
+    n = int(np.prod(dims))
+    E = 64 * n * len(dims) + 28
+    V = np.random.default_rng(n).standard_normal((n, E), dtype=np.float32)
+    seg, blk = placement_labels(E, dims)
+    plan = T.trivance_plan(dims, "B", placement="schedule")
+    S = plan.num_steps
+    _say(f"[placed step hook] dims={dims} E={E}")
+    buf = torch.from_numpy(V).cuda()
+    T.trivance_allreduce_emulated_steps(buf, plan, 0, S)
+    torch.cuda.synchronize()
+    want_rs = allreduce.bandwidth_optimal(V, dims, col_seg=seg, col_blk=blk, ag_passes=0)
+    np.testing.assert_array_equal(buf.cpu().numpy(), want_rs)
+    T.trivance_allreduce_emulated_steps(buf, plan, S, 2 * S)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(buf.cpu().numpy(),
+                                  allreduce.bandwidth_optimal(V, dims, col_seg=seg, col_blk=blk))

@@ -28,7 +28,7 @@ def _say(msg):
 def _run_full(w, V):
     import paper_2602_17254_amd as T
 
-    plan = T.trivance_plan(w.dims, w.variant)
+    plan = T.trivance_plan(w.dims, w.variant, w.placement)
     buf = torch.from_numpy(V).cuda()
     T.trivance_allreduce_emulated(buf, plan)
     torch.cuda.synchronize()
@@ -37,7 +37,8 @@ def _run_full(w, V):
 
 def _check_sampled(w, V, buf, seed):
     D = len(w.dims)
-    cols, seg, blk = sample_columns(w.elems, D, w.n, w.variant, seed)
+    cols, seg, blk = sample_columns(w.elems, D, w.n, w.variant, seed, dims=w.dims,
+                                    placement=w.placement)
     idx = torch.from_numpy(cols).cuda()
     got = buf.index_select(1, idx).cpu().numpy()
     return assert_matches_oracle(got, np.ascontiguousarray(V[:, cols]), w.dims, w.variant,
@@ -150,10 +151,11 @@ def _device_hash_workload(w, max_blocks=None):
     D = len(w.dims)
     buf = torch.empty((w.n, w.elems), dtype=torch.float32, device="cuda")
     T.trivance_fill_hash_uniform(buf, w.seed)
-    plan = T.trivance_plan(w.dims, w.variant)
+    plan = T.trivance_plan(w.dims, w.variant, w.placement)
     T.trivance_allreduce_emulated(buf, plan)
     torch.cuda.synchronize()
-    cols, seg, blk = sample_columns(w.elems, D, w.n, w.variant, w.seed, max_blocks=max_blocks)
+    cols, seg, blk = sample_columns(w.elems, D, w.n, w.variant, w.seed, max_blocks=max_blocks,
+                                    dims=w.dims, placement=w.placement)
     got = buf.index_select(1, torch.from_numpy(cols).cuda()).cpu().numpy()
     Vs = inputs.hash_uniform(w.seed, w.elems, np.arange(w.n), cols)
     assert_matches_oracle(got, Vs, w.dims, w.variant, col_seg=seg, col_blk=blk, what=w.name)
@@ -181,3 +183,38 @@ def test_torus16x16x16_bandwidth_8MiB_nonpower3():
     _say(f"[workload] {w.name} f32, device-generated inputs (column sample of 64 blocks per "
          "segment)")
     _device_hash_workload(w, max_blocks=64)
+
+
+# The power-of-three bandwidth-optimal workloads with message-contiguous block placement: the
+# same column sample, labelled with the block placed at each column's granule range.
+def test_ring243_bandwidth_32MiB_placed():
+    w = inputs.WORKLOADS["ring243_Bp_32MiB"]
+    _say(f"[workload] {w.name} f32 (column sample)")
+    V = inputs.normal_f32(w.seed, w.n, w.elems)
+    buf = _run_full(w, V)
+    _check_sampled(w, V, buf, seed=w.seed)
+    del buf
+    _say(f"[workload] {w.name} i32 (column sample)")
+    Vi = inputs.uniform_i32(w.int_seed, w.n, w.elems, *w.int_range)
+    buf = _run_full(w, Vi)
+    _check_sampled(w, Vi, buf, seed=w.int_seed)
+    assert bool((buf[1:] == buf[0:1]).all().item())
+    del buf
+    torch.cuda.empty_cache()
+
+
+def test_torus27x27_bandwidth_4MiB_placed():
+    w = inputs.WORKLOADS["torus27x27_Bp_4MiB"]
+    _say(f"[workload] {w.name} f32 (column sample)")
+    V = inputs.normal_f32(w.seed, w.n, w.elems)
+    buf = _run_full(w, V)
+    _check_sampled(w, V, buf, seed=w.seed)
+    assert bool((buf[1:] == buf[0:1]).all().item())
+    del buf
+    torch.cuda.empty_cache()
+
+
+def test_torus9x9x9_bandwidth_128MiB_placed():
+    w = inputs.WORKLOADS["torus9x9x9_Bp_128MiB"]
+    _say(f"[workload] {w.name} f32, device-generated inputs (column sample)")
+    _device_hash_workload(w)

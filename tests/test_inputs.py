@@ -38,7 +38,15 @@ def test_hash_uniform_grid_and_range():
 def test_workload_table():
     w = inputs.WORKLOADS
     assert inputs.HEADLINE in w
-    assert [x.n for x in w.values()] == [9, 81, 243, 729, 729, 8, 64, 1024, 512, 4096]
+    assert [x.n for x in w.values()] == [9, 81, 243, 729, 729, 8, 64, 1024, 512, 4096,
+                                         243, 729, 729]
+    placed = [x for x in w.values() if x.placement == "schedule"]
+    assert [x.name for x in placed] == ["ring243_Bp_32MiB", "torus27x27_Bp_4MiB",
+                                        "torus9x9x9_Bp_128MiB"]
+    for x in placed:  # same inputs as the default-partition workload of the same shape and size
+        twin = w[x.name.replace("_Bp_", "_B_")]
+        assert (twin.dims, twin.elems, twin.dist, twin.seed, twin.int_range) == \
+            (x.dims, x.elems, x.dist, x.seed, x.int_range) and twin.placement == "natural"
     assert w["torus9x9x9_B_128MiB"].rank_bytes == 128 * 2 ** 20
     assert w["ring81_L_8MiB"].rank_bytes == 8 * 2 ** 20
     a = inputs.normal_f32(1, 3, 10)
