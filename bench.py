@@ -331,6 +331,8 @@ def copy_probe(nbytes: int, reps: int = 3) -> None:
 
 SWEEP_CLASSES = [((81,), "L"), ((243,), "B"), ((27, 27), "B"), ((9, 9, 9), "B"), ((8,), "B"),
                  ((64,), "B"), ((32, 32), "B"), ((8, 64), "B"), ((16, 16, 16), "B")]
+# the power-of-three bandwidth-optimal classes again with message-contiguous block placement
+SWEEP_PLACED = [(243,), (27, 27), (9, 9, 9)]
 SWEEP_MIB = [8, 16, 32, 64, 128]
 SWEEP_MAX_RESIDENT = 150 * 2 ** 30  # 16x16x16 stops at 32 MiB per rank (128 GiB resident)
 
@@ -343,14 +345,16 @@ def sweep(steps: int, warmup: int) -> None:
     import paper_2602_17254_amd as T
 
     torch.cuda.set_device(0)
-    for dims, variant in SWEEP_CLASSES:
-        plan = T.trivance_plan(dims, variant)
+    classes = [(d, v, "natural") for d, v in SWEEP_CLASSES] + \
+              [(d, "B", "schedule") for d in SWEEP_PLACED]
+    for dims, variant, placement in classes:
+        plan = T.trivance_plan(dims, variant, placement)
         n = plan.n
         for mib in SWEEP_MIB:
             E = mib * 2 ** 20 // 4
             if n * E * 4 > SWEEP_MAX_RESIDENT:
                 continue
-            _say(f"[sweep] {'x'.join(map(str, dims))} {variant} {mib} MiB per rank")
+            _say(f"[sweep] {'x'.join(map(str, dims))} {variant} {placement} {mib} MiB per rank")
             buf = torch.empty((n, E), dtype=torch.float32, device="cuda")
             T.trivance_fill_hash_uniform(buf, 7)
             for _ in range(warmup):
@@ -364,7 +368,7 @@ def sweep(steps: int, warmup: int) -> None:
             alg = T.trivance_algorithmic_bytes(plan, E)
             gbps = alg / (ms * 1e-3) / 1e9
             print(json.dumps({"sweep": "x".join(map(str, dims)), "variant": variant,
-                              "rank_mib": mib, "n_ranks": n, "passes": plan.num_passes,
+                              "block_placement": placement, "rank_mib": mib, "n_ranks": n, "passes": plan.num_passes,
                               "ms_per_allreduce": round(ms, 4), "GBps": round(gbps, 1),
                               "pct_of_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
                               "resident_GB": round(n * E * 4 / 1e9, 2)}), flush=True)
