@@ -43,6 +43,16 @@ int main(void) {
     CHECK(trivance_plan_step(q, 1, 0, NULL, NULL, NULL, &distance) == TRIVANCE_OK && distance == 3);
     trivance_plan_destroy(q);
 
+    /* message-contiguous placement: on a 27-ring block 1 lies at position 9 (digits reversed) */
+    trivance_plan_t* pl = NULL;
+    CHECK(trivance_plan_ex(27, NULL, 0, TRIVANCE_BANDWIDTH_OPT, TRIVANCE_PLACE_BY_SCHEDULE, &pl) ==
+          TRIVANCE_OK);
+    CHECK(trivance_block_range(pl, 27 * 64, 0, 1, &b, &e) == TRIVANCE_OK && b == 576 && e == 640);
+    trivance_plan_destroy(pl);
+    CHECK(trivance_plan_ex(27, NULL, 0, TRIVANCE_LATENCY_OPT, TRIVANCE_PLACE_BY_SCHEDULE, &pl) ==
+          TRIVANCE_EUNSUPPORTED);
+    CHECK(trivance_plan_ex(27, NULL, 0, TRIVANCE_BANDWIDTH_OPT, 4u, &pl) == TRIVANCE_EINVAL);
+
     /* errors */
     trivance_plan_t* r = NULL;
     CHECK(trivance_plan(8, NULL, 0, TRIVANCE_LATENCY_OPT, &r) == TRIVANCE_EUNSUPPORTED && r == NULL);
