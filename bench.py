@@ -40,24 +40,30 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # source it was measured on (sha256 of the source file, first 16 hex digits).
 MEASURED_TRAFFIC = {
     # profiles/<kernel>_<workload>.md
-    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "b35e3a5e28b944d4",
-        "bytes_per_launch": 1359026675},
-    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "b35e3a5e28b944d4",
-        "bytes_per_launch": 3248084375},
-    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "b35e3a5e28b944d4",
-        "bytes_per_launch": 1017881747},
-    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "b35e3a5e28b944d4",
-        "bytes_per_launch": 32569687256},
-    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "b35e3a5e28b944d4",
-        "bytes_per_launch": 251705637},
-    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b35e3a5e28b944d4",
-        "bytes_per_launch": 283162772},
-    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b35e3a5e28b944d4",
-        "bytes_per_launch": 2286971773},
-    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b35e3a5e28b944d4",
-        "bytes_per_launch": 1550530307},
-    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b35e3a5e28b944d4",
-        "bytes_per_launch": 9724133542},
+    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "2450085788fe37cb",
+        "bytes_per_launch": 1359039931},
+    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
+        "bytes_per_launch": 3248090830},
+    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
+        "bytes_per_launch": 1017891161},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
+        "bytes_per_launch": 32569646337},
+    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
+        "bytes_per_launch": 251705389},
+    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
+        "bytes_per_launch": 283162398},
+    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
+        "bytes_per_launch": 2286967862},
+    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
+        "bytes_per_launch": 1550527749},
+    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
+        "bytes_per_launch": 9724181357},
+    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
+        "bytes_per_launch": 3248093765},
+    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
+        "bytes_per_launch": 1017894702},
+    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
+        "bytes_per_launch": 32569534892},
 }
 
 
