@@ -457,6 +457,27 @@ def test_parity_placed(dims, E, dtype):
         np.testing.assert_array_equal(got, np.broadcast_to(allreduce.exact_int_sum(V), got.shape))
 
 
+@pytest.mark.parametrize("dims", [(9,), (3, 3)])
+def test_placed_misaligned_rows_use_scalar_path(dims):
+    """Placed plans on a [n, E] view whose start is not 16-byte aligned (4-byte accesses)."""
+    import paper_2602_17254_amd as T
+    from gpu_util import placement_labels
+
+    n = int(np.prod(dims))
+    E = 64 * n * len(dims) * 2 + 8
+    V = np.random.default_rng(5).standard_normal((n, E), dtype=np.float32)
+    _say(f"[placed misaligned] dims={dims}")
+    flat = torch.zeros(n * E + 1, dtype=torch.float32, device="cuda")
+    view = flat[1:].view(n, E)
+    view.copy_(torch.from_numpy(V))
+    assert view.data_ptr() % 16 != 0
+    T.trivance_allreduce_emulated(view, T.trivance_plan(dims, "B", placement="schedule"))
+    torch.cuda.synchronize()
+    seg, blk = placement_labels(E, dims)
+    assert_matches_oracle(view.cpu().numpy(), V, dims, "B", col_seg=seg, col_blk=blk,
+                          what="placed misaligned")
+
+
 @pytest.mark.parametrize("dims", [(27,), (9, 9), (3, 3, 3)])
 def test_placed_step_hook_reduce_scatter_then_resume(dims):
     """Placed plans: the state after the reduce-scatter passes equals the oracle's, and resuming
