@@ -110,10 +110,11 @@ int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance
  *   flags  0, or TRIVANCE_PLACE_BY_SCHEDULE: block j of every segment lies at the granule range of
  *          position pos_c(j) instead of the j-th one (see trivance_block_range). pos_c(j) spells
  *          the base-3 digits of block j's coordinates in the order collective c's steps fix them
- *          (step t fixes digit t div D of dimension (c + t) mod D), most significant first. The
- *          blocks a rank keeps after each reduce-scatter step (Sec. 4.3 closed form) and every
- *          message are then one contiguous range of positions. Power-of-three sides of equal
- *          length, bandwidth-optimal variant only (EUNSUPPORTED otherwise). The option changes
+ *          (each step fixes the next digit of the coordinate of the dimension it works on; with
+ *          equal sides step t fixes digit t div D of dimension (c + t) mod D), most significant
+ *          first. The blocks a rank keeps after each reduce-scatter step (Sec. 4.3 closed form)
+ *          and every message are then one contiguous range of positions. Power-of-three sides,
+ *          bandwidth-optimal variant only (EUNSUPPORTED otherwise). The option changes
  *          which elements share a block, hence an element's fp32 summation tree; int32 results
  *          are the same exact sums.
  * Errors: those of trivance_plan, and EINVAL for unknown flag bits.

@@ -14,7 +14,7 @@ a torus). Under this placement those blocks, and therefore every message, occupy
 run of positions. The floating-point summation tree of an element depends on which block it lies
 in, so results differ in fp32 bits from the default partition (not in int32).
 
-Only ranks of equal power-of-three sides use it (the option is rejected elsewhere).
+Only power-of-three sides use it (equal or not; the option is rejected elsewhere).
 """
 
 from __future__ import annotations

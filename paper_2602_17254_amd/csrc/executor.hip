@@ -58,6 +58,9 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t x, const FastDiv& f) {
     return __umulhi(x << 1, f.mul) >> f.shift;
 }
 
+// Base-3 digits of a block index of a power-of-three plan (n < 2^31, so at most 19).
+constexpr int kMaxPlacedDigits = 20;
+
 struct StepArgs {
     int64_t elems;                 // elements per rank row
     int64_t seg_g[kMaxDims + 1];   // segment granule starts, seg_g[D] = total granules
@@ -85,9 +88,13 @@ struct StepArgs {
     FastDiv f_nq[kMaxDims][kMaxDims];    // dims[d] / modulus[c][d]
     uint32_t wg_base;              // first workgroup of this dispatch (for_each_dispatch)
     // block steps of plans placed by schedule digits (TRIVANCE_PLACE_BY_SCHEDULE)
+    // (32-bit words: the scalar unit loads them directly; bytes would go through vector loads)
     int placed;
-    int S;                                 // steps per phase
-    uint8_t pdig[kMaxDims][kMaxDims];     // digits of dimension d that collective c has fixed
+    uint32_t pdig[kMaxDims][kMaxDims];    // digits of dimension d that collective c has fixed
+    uint32_t pexp_off[kMaxDims];          // first entry of dimension d in pexp[c]
+    uint32_t pexp[kMaxDims][kMaxPlacedDigits / 4];  // entry i of collective c: byte i % 4 of
+                                                     // word i / 4; entry pexp_off[d] + k is the
+                                                     // position exponent of digit k of dimension d
 };
 
 template <typename T, int N>
@@ -340,8 +347,8 @@ __device__ __forceinline__ bool decode_unit(const StepArgs& a, uint32_t unit, in
     uint32_t j = 0, rr = r, r_act = 0;
     if (a.placed) {
         // the centre keeps the blocks that agree with it in the digits fixed so far, which sit
-        // at one run of positions: the centre's own fixed digits, most significant first (digit
-        // k of dimension d was fixed at step k D + ((d - c) mod D)), then q
+        // at one run of positions: the centre's own fixed digits, each at the weight 3^(S - 1 -
+        // the step that fixed it), then q
         const uint32_t q0 = q;
 #pragma unroll
         for (int d = 0; d < kMaxDims; ++d) {
@@ -350,10 +357,11 @@ __device__ __forceinline__ bool decode_unit(const StepArgs& a, uint32_t unit, in
                 uint32_t x = rr - rr_next * (uint32_t)a.dims[d];
                 rr = rr_next;
                 if (d == act) r_act = x;
-                const int delta = d >= (int)c ? d - (int)c : d + a.D - (int)c;
-                int e = a.S - 1 - delta;
-                for (int k = 0; k < (int)a.pdig[c][d]; ++k, e -= a.D) {
+                const uint32_t base = a.pexp_off[d];
+                for (uint32_t k = 0; k < a.pdig[c][d]; ++k) {
                     const uint32_t x3 = __umulhi(x, 0xAAAAAAABu) >> 1;  // x / 3
+                    const uint32_t i = base + k;
+                    const uint32_t e = (a.pexp[c][i >> 2] >> (8 * (i & 3))) & 0xFFu;
                     j += (x - 3u * x3) * kPow3[e];
                     x = x3;
                 }
@@ -745,7 +753,23 @@ inline int base_args(const trivance_plan_t* p, int64_t elems, StepArgs* out, int
     a.narrow = (int64_t)p->n * (max_gc + 1) < ((int64_t)1 << 31) ? 1 : 0;
     a.f_n = make_fastdiv((uint32_t)p->n);
     a.placed = p->placed ? 1 : 0;
-    a.S = p->S;
+    if (p->placed) {
+        // position exponent S - 1 - t of the digit that reduce-scatter step t fixes
+        int off = 0;
+        for (int d = 0; d < p->D; ++d) {
+            a.pexp_off[d] = (uint32_t)off;
+            for (int v = p->dims[d]; v > 1; v /= 3) ++off;
+        }
+        if (off > kMaxPlacedDigits || p->S != off) return TRIVANCE_EUNSUPPORTED;
+        for (int c = 0; c < p->D; ++c) {
+            int taken[kMaxDims] = {};
+            for (int t = 0; t < p->S; ++t) {
+                const int d = p->passes[t].dim[c];
+                const uint32_t i = a.pexp_off[d] + (uint32_t)taken[d]++;
+                a.pexp[c][i >> 2] |= (uint32_t)(p->S - 1 - t) << (8 * (i & 3));
+            }
+        }
+    }
     for (int d = 0; d < kMaxDims; ++d) a.f_side[d] = make_fastdiv((uint32_t)a.dims[d]);
     *max_blk = max_block_granules(p, elems) * kGranule;
     if (*max_blk >= ((int64_t)1 << 31)) return TRIVANCE_EUNSUPPORTED;
@@ -767,7 +791,7 @@ inline int pass_args(const trivance_plan_t* p, const Pass& ps, int64_t max_blk, 
             a->f_nq[c][d] = make_fastdiv((uint32_t)(a->dims[d] / m));
             int digits = 0;
             for (int v = m; v > 1; v /= 3) ++digits;
-            a->pdig[c][d] = (uint8_t)digits;
+            a->pdig[c][d] = (uint32_t)digits;
         }
     }
     a->kept = (int)ps.kept_per_rank;

@@ -280,8 +280,8 @@ int build_tree_plan(trivance_plan_t* p) {
 namespace trivance {
 
 int placed_position(const trivance_plan_t* p, int c, int block) {
-    // equal sides: step t of collective c works on dimension (c + t) mod D and fixes the next
-    // digit (digit t div D) of that coordinate
+    // reduce-scatter step t (pass t) of collective c works on dimension passes[t].dim[c] and
+    // fixes that coordinate's next base-3 digit
     int coord[kMaxDims];
     int rest = block;
     for (int d = 0; d < p->D; ++d) {
@@ -290,7 +290,7 @@ int placed_position(const trivance_plan_t* p, int c, int block) {
     }
     int pos = 0;
     for (int t = 0; t < p->S; ++t) {
-        const int d = (c + t) % p->D;
+        const int d = p->passes[t].dim[c];
         pos = 3 * pos + coord[d] % 3;
         coord[d] /= 3;
     }
@@ -368,11 +368,8 @@ int trivance_plan_ex(int n, const int* torus_dims, int ndims, int variant, unsig
     }
     bool pow3 = true;
     for (int d = 0; d < D; ++d) pow3 = pow3 && log3_exact(dims[d]) >= 0;
-    if (flags & TRIVANCE_PLACE_BY_SCHEDULE) {
-        bool equal = true;
-        for (int d = 1; d < D; ++d) equal = equal && dims[d] == dims[0];
-        if (!pow3 || !equal || variant != TRIVANCE_BANDWIDTH_OPT) return TRIVANCE_EUNSUPPORTED;
-    }
+    if ((flags & TRIVANCE_PLACE_BY_SCHEDULE) && (!pow3 || variant != TRIVANCE_BANDWIDTH_OPT))
+        return TRIVANCE_EUNSUPPORTED;
     // Sec. 4.4 (sides that are not powers of three): bandwidth-optimal variant only
     if (!pow3) {
         if (variant != TRIVANCE_BANDWIDTH_OPT || D > trivance::kMaxTreeDims)

@@ -108,7 +108,9 @@ def test_plan_errors():
 
 
 @pytest.mark.parametrize("dims,E", [((9,), 64 * 9 * 3 + 20), ((243,), 8 * 2 ** 20), ((27, 27), 1_048_576),
-                                    ((9, 9, 9), 12345), ((3, 3, 3, 3), 5000), ((1,), 100)])
+                                    ((9, 9, 9), 12345), ((3, 3, 3, 3), 5000), ((1,), 100),
+                                    ((3, 9), 5000), ((27, 3), 64 * 81 * 2 + 4), ((3, 3, 9), 7777),
+                                    ((9, 27), 64 * 243 * 2), ((1, 9), 999)])
 def test_placed_block_range_matches_oracle_placement(dims, E):
     from oracle import placement
 
@@ -123,7 +125,7 @@ def test_placed_block_range_matches_oracle_placement(dims, E):
 
 def test_placement_is_rejected_where_it_does_not_apply():
     lib = T.binding._lib()
-    for dims, variant in [((8,), "B"), ((9, 27), "B"), ((9,), "L"), ((9,), "BRUCK"), ((4, 4), "B")]:
+    for dims, variant in [((8,), "B"), ((9,), "L"), ((9,), "BRUCK"), ((4, 4), "B"), ((3, 8), "B")]:
         with pytest.raises(T.TrivanceError) as e:
             T.trivance_plan(dims, variant, placement="schedule")
         assert e.value.status == -2

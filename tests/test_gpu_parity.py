@@ -428,13 +428,16 @@ def test_graph_capture_replays(dims, variant):
         assert torch.equal(buf, eager), f"replay {k} differs from the eager result"
 
 
-# Message-contiguous block placement (TRIVANCE_PLACE_BY_SCHEDULE): bandwidth-optimal, equal
+# Message-contiguous block placement (TRIVANCE_PLACE_BY_SCHEDULE): bandwidth-optimal,
 # power-of-three sides; against the oracle with the placed block labels
 PLACED = [((3,), 64 * 3 * 5 + 4), ((9,), 7), ((9,), 64 * 9 * 3 + 20), ((27,), 5003),
           ((81,), 64 * 81 * 2 + 8), ((243,), 64 * 243 * 2 + 4), ((729,), 64 * 729 + 8),
           ((3, 3), 3333), ((9, 9), 64 * 81 * 3 + 4), ((27, 27), 64 * 729 + 36),
           ((3, 3, 3), 64 * 27 * 3 + 16), ((9, 9, 9), 64 * 729 * 2 + 100),
-          ((3, 3, 3, 3), 64 * 81 * 4 + 12), ((1,), 5), ((9,), 0)]
+          ((3, 3, 3, 3), 64 * 81 * 4 + 12), ((1,), 5), ((9,), 0),
+          # unequal sides (the step order of the rotation reading)
+          ((3, 9), 64 * 27 * 3 + 4), ((9, 3), 777), ((3, 27), 64 * 81 * 2 + 12),
+          ((3, 3, 9), 64 * 81 * 2 + 4), ((9, 27), 64 * 243 + 4), ((1, 9), 64 * 9 * 2 + 4)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "i32"])

@@ -13,7 +13,7 @@ import pytest
 from oracle import allreduce, partition, placement, schedule
 
 SHAPES = [(3,), (9,), (27,), (81,), (243,), (3, 3), (9, 9), (27, 27), (3, 3, 3), (9, 9, 9),
-          (3, 3, 3, 3)]
+          (3, 3, 3, 3), (3, 9), (27, 3), (3, 3, 9), (9, 27)]
 
 
 def _digits_reversed(j: int, s: int) -> int:
@@ -45,7 +45,8 @@ def _kept_after(torus, c, r, t):
     return kept
 
 
-@pytest.mark.parametrize("dims", [(9,), (27,), (81,), (3, 3), (9, 9), (3, 3, 3), (3, 3, 3, 3)],
+@pytest.mark.parametrize("dims", [(9,), (27,), (81,), (3, 3), (9, 9), (3, 3, 3), (3, 3, 3, 3),
+                                  (3, 9), (9, 3), (3, 27), (3, 3, 9)],
                          ids=lambda d: "x".join(map(str, d)))
 def test_kept_sets_and_messages_are_contiguous(dims):
     torus = schedule.Torus(dims)
@@ -72,7 +73,8 @@ def test_natural_order_is_not_contiguous():
 
 @pytest.mark.parametrize("dims,E", [((9,), 64 * 9 * 3 + 20), ((27,), 64 * 27 * 2 + 4),
                                     ((3, 3), 64 * 9 * 4 + 12), ((9, 9), 64 * 81 * 2 + 4),
-                                    ((3, 3, 3), 64 * 27 * 3 + 16)],
+                                    ((3, 3, 3), 64 * 27 * 3 + 16), ((3, 9), 64 * 27 * 2 + 8),
+                                    ((9, 3, 3), 777)],
                          ids=lambda x: "x".join(map(str, x)) if isinstance(x, tuple) else str(x))
 def test_allreduce_under_placement(dims, E):
     n = int(np.prod(dims))
