@@ -1,5 +1,6 @@
 """Host-side logic of bench.py (no GPU): phase grouping of the timed region, the power-of-three
-test that picks the kernel family, the CPU-baseline column sample and the --gpus refusal."""
+test that picks the kernel family, the CPU-baseline column sample and its repetition, and the
+--gpus refusal."""
 
 import subprocess
 import sys
@@ -47,3 +48,24 @@ def test_more_than_one_gpu_is_refused():
                          text=True, timeout=120)
     assert res.returncode == 2
     assert "one GPU" in res.stderr
+
+
+@pytest.mark.parametrize("name", ["ring9_L_4KiB", "ring243_B_32MiB", "ring243_Bp_32MiB"])
+def test_cpu_baseline_repeats_short_samples(name):
+    """The baseline reruns a short sample up to the time target (capped), reports the number of
+    runs and compares the first result: here the oracle's own, so it must match."""
+    from oracle import allreduce, partition, placement
+
+    w = inputs.WORKLOADS[name]
+    cols = bench._sample_for_baseline(w, min(300, w.elems))
+    V_cols = np.random.default_rng(w.seed).standard_normal((w.n, cols.size), dtype=np.float32)
+    if w.placement == "schedule":
+        seg, blk = placement.column_labels(w.elems, w.dims, cols)
+    else:
+        seg, blk = partition.column_labels(w.elems, len(w.dims), w.n, cols)
+    first = (allreduce.latency_optimal(V_cols, w.dims, col_seg=seg) if w.variant == "L" else
+             allreduce.allreduce(V_cols, w.dims, "B", col_seg=seg, col_blk=blk))
+    out = bench.cpu_baseline(w, first, cols, V_cols, seconds_target=0.05, max_runs=3)
+    assert 1 <= out["runs"] <= 3 and out["matches_gpu_on_sample"] is True
+    assert out["value"] > 0 and out["cores"] == 1 and f"{out['runs']} run(s)" in out["sample"]
+    assert out["gpu_fp64_bound_ratio_on_sample"] <= 1.0
