@@ -40,30 +40,30 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # source it was measured on (sha256 of the source file, first 16 hex digits).
 MEASURED_TRAFFIC = {
     # profiles/<kernel>_<workload>.md
-    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "2450085788fe37cb",
-        "bytes_per_launch": 1359039931},
-    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
-        "bytes_per_launch": 3248090830},
-    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
-        "bytes_per_launch": 1017891161},
-    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
-        "bytes_per_launch": 32569646337},
-    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
-        "bytes_per_launch": 251705389},
-    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
-        "bytes_per_launch": 283162398},
-    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
-        "bytes_per_launch": 2286967862},
-    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
-        "bytes_per_launch": 1550527749},
-    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
-        "bytes_per_launch": 9724181357},
-    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
-        "bytes_per_launch": 3248093765},
-    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
-        "bytes_per_launch": 1017894702},
-    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {"src_sha": "2450085788fe37cb",
-        "bytes_per_launch": 32569534892},
+    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "016f2ebe2a7c8ff3",
+        "bytes_per_launch": 1359035299},
+    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
+        "bytes_per_launch": 3248090550},
+    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
+        "bytes_per_launch": 1017890946},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
+        "bytes_per_launch": 32569525591},
+    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
+        "bytes_per_launch": 251705480},
+    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
+        "bytes_per_launch": 283162172},
+    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
+        "bytes_per_launch": 2286967360},
+    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
+        "bytes_per_launch": 1550526138},
+    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
+        "bytes_per_launch": 9724116032},
+    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
+        "bytes_per_launch": 3248094330},
+    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
+        "bytes_per_launch": 1017897232},
+    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
+        "bytes_per_launch": 32569639077},
 }
 
 
