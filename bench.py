@@ -137,6 +137,15 @@ def cpu_baseline(w, gpu_first_result_cols, cols, V_cols, seconds_target=10.0, ma
         err = np.abs(gpu_first_result_cols.astype(np.float64) - allreduce.fp64_sum(V_cols)[None, :])
         bound = np.maximum(allreduce.fp32_error_bound(V_cols, S)[None, :], 1e-300)
         exact = {"gpu_fp64_bound_ratio_on_sample": round(float((err / bound).max()), 4)}
+    import torch
+
+    if w.congestion and torch.cuda.is_available():
+        # the per-link message counts of the plan, GPU counter against the oracle's link walk
+        from oracle import congestion
+
+        got = T.trivance_congestion(T.trivance_plan(w.dims, w.variant, w.placement))
+        exact["congestion_exact"] = bool(np.array_equal(got, congestion.link_loads(w.dims,
+                                                                                  w.variant)))
     return {
         "value": round(sample_bytes * runs / dt / 1e9, 4),
         "unit": "GB/s",
