@@ -1,6 +1,7 @@
 /* End-to-end use of the C ABI from plain C on the GPU (HIP runtime API for memory, no Python):
- * int32 AllReduces on a ring (latency- and bandwidth-optimal), a torus and a ring of 8 are
- * checked against exact column sums; congestion loads against 3^k. Exit status 0 on success. */
+ * int32 AllReduces on a ring (latency- and bandwidth-optimal), a torus and a ring of 8, and two
+ * with the message-contiguous block placement, are checked against exact column sums; congestion
+ * loads against 3^k. Exit status 0 on success. */
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 #include <stdio.h>
@@ -17,9 +18,10 @@ static int failures = 0;
         }                                                                                \
     } while (0)
 
-static void run_case(int n, const int* dims, int ndims, int variant, int64_t elems) {
+static void run_case(int n, const int* dims, int ndims, int variant, unsigned flags,
+                     int64_t elems) {
     trivance_plan_t* plan = NULL;
-    if (trivance_plan(n, dims, ndims, variant, &plan) != TRIVANCE_OK) {
+    if (trivance_plan_ex(n, dims, ndims, variant, flags, &plan) != TRIVANCE_OK) {
         CHECK(0);
         return;
     }
@@ -53,10 +55,13 @@ static void run_case(int n, const int* dims, int ndims, int variant, int64_t ele
 
 int main(void) {
     int ring27[1] = {27}, torus[2] = {9, 9}, ring8[1] = {8};
-    run_case(27, ring27, 1, TRIVANCE_LATENCY_OPT, 64 * 27 * 2 + 4);
-    run_case(27, ring27, 1, TRIVANCE_BANDWIDTH_OPT, 64 * 27 * 3 + 7);
-    run_case(81, torus, 2, TRIVANCE_BANDWIDTH_OPT, 64 * 81 * 2 * 2 + 12);
-    run_case(8, ring8, 1, TRIVANCE_BANDWIDTH_OPT, 64 * 8 * 4 + 3);
+    run_case(27, ring27, 1, TRIVANCE_LATENCY_OPT, 0u, 64 * 27 * 2 + 4);
+    run_case(27, ring27, 1, TRIVANCE_BANDWIDTH_OPT, 0u, 64 * 27 * 3 + 7);
+    run_case(81, torus, 2, TRIVANCE_BANDWIDTH_OPT, 0u, 64 * 81 * 2 * 2 + 12);
+    run_case(8, ring8, 1, TRIVANCE_BANDWIDTH_OPT, 0u, 64 * 8 * 4 + 3);
+    /* the message-contiguous block placement */
+    run_case(27, ring27, 1, TRIVANCE_BANDWIDTH_OPT, TRIVANCE_PLACE_BY_SCHEDULE, 64 * 27 * 3 + 7);
+    run_case(81, torus, 2, TRIVANCE_BANDWIDTH_OPT, TRIVANCE_PLACE_BY_SCHEDULE, 64 * 81 * 4 + 12);
 
     /* congestion of the 27-ring, latency-optimal: every directed link carries 3^k in pass k */
     trivance_plan_t* plan = NULL;
