@@ -717,11 +717,11 @@ __global__ __launch_bounds__(kBlockThreads) void tree_step_kernel(T* __restrict_
 // whole workgroups (for_each_dispatch), each with its first workgroup in the argument block.
 template <typename T, typename Args>
 hipError_t dispatch(void (*kernel)(T*, Args), uint64_t grid, int threads, hipStream_t stream,
-                    T* buf, Args a) {
+                    T* buf, Args a, size_t dynamic_lds = 0) {
     hipError_t err = hipSuccess;
     for_each_dispatch(grid, threads, [&](uint32_t first, uint32_t count) {
         a.wg_base = first;
-        hipLaunchKernelGGL(kernel, dim3(count), dim3(threads), 0, stream, buf, a);
+        hipLaunchKernelGGL(kernel, dim3(count), dim3(threads), dynamic_lds, stream, buf, a);
         err = hipGetLastError();
         return err == hipSuccess;
     });
@@ -833,11 +833,27 @@ inline void set_columns(StepArgs* a, Launch* L, int cols) {
     L->grid = (uint32_t)((int64_t)L->ncoll * a->ncycles * a->colblocks);
 }
 
+// LDS of one MI355X compute unit. A workgroup that asks for 1/k of it leaves room for k
+// workgroups at most; the latency tiles use this to cap how many cycles a CU streams at once.
+constexpr size_t kLdsPerCu = 160 * 1024;
+
+// Resident workgroups per CU for each latency tile (0: no cap), measured best on MI355X over the
+// 81- and 243-rings, 27x27 and 9x9x9 at 8 MiB per rank. Fewer concurrent cycles keep fewer rows
+// streaming at once; tiles whose waves walk many rows keep enough bytes in flight with one
+// workgroup per CU, while the 27-row tile (3 rows per wave) needs the full occupancy.
+template <int SUB, int P>
+constexpr int latency_wg_per_cu() {
+    return (SUB == 3 && P == 1) ? 16 : (SUB == 3 && P == 3) ? 4 : (SUB == 3 && P == 9) ? 0 : 1;
+}
+
 template <typename T, int VEC, int SUB, int P, bool XCD = false>
 hipError_t launch_split(T* buf, StepArgs a, Launch L, hipStream_t stream) {
     set_columns(&a, &L, 64);
+    constexpr int cap = latency_wg_per_cu<SUB, P>();
+    constexpr size_t halo = (size_t)P * 2 * 64 * sizeof(Vec<T, VEC>);  // the kernel's own LDS
+    constexpr size_t extra = cap ? kLdsPerCu / cap - halo - 256 : 0;   // unused, caps occupancy
     return dispatch(latency_split_kernel<T, VEC, SUB, P, 1, true, XCD>, L.grid, 64 * P, stream,
-                    buf, a);
+                    buf, a, extra);
 }
 
 template <typename T, int VEC>
