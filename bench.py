@@ -40,30 +40,30 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # source it was measured on (sha256 of the source file, first 16 hex digits).
 MEASURED_TRAFFIC = {
     # profiles/<kernel>_<workload>.md
-    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "016f2ebe2a7c8ff3",
-        "bytes_per_launch": 1359035299},
-    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
-        "bytes_per_launch": 3248090550},
-    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
-        "bytes_per_launch": 1017890946},
-    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
-        "bytes_per_launch": 32569525591},
-    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
-        "bytes_per_launch": 251705480},
-    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
-        "bytes_per_launch": 283162172},
-    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
-        "bytes_per_launch": 2286967360},
-    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
-        "bytes_per_launch": 1550526138},
-    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
-        "bytes_per_launch": 9724116032},
-    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
-        "bytes_per_launch": 3248094330},
-    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
-        "bytes_per_launch": 1017897232},
-    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {"src_sha": "016f2ebe2a7c8ff3",
-        "bytes_per_launch": 32569639077},
+    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "efca26cfa1b94003",
+        "bytes_per_launch": 1359214600},
+    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
+        "bytes_per_launch": 3248090325},
+    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
+        "bytes_per_launch": 1017890817},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
+        "bytes_per_launch": 32569524620},
+    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
+        "bytes_per_launch": 251705451},
+    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
+        "bytes_per_launch": 283162324},
+    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
+        "bytes_per_launch": 2286967203},
+    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
+        "bytes_per_launch": 1550526050},
+    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
+        "bytes_per_launch": 9724115763},
+    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
+        "bytes_per_launch": 3248094362},
+    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
+        "bytes_per_launch": 1017897280},
+    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
+        "bytes_per_launch": 32569529737},
 }
 
 
