@@ -259,14 +259,14 @@ __global__ __launch_bounds__(kBlockThreads) void latency_step_kernel(T* __restri
 // wave publishes its own first and last row in LDS and reads its neighbours' after one barrier,
 // before any store, so the in-place update stays correct. Splitting gives P times more, P times
 // shorter wavefronts than walking the whole cycle in one wavefront.
-template <typename T, int VEC, int SUB, int P, int PD, bool NT, bool XCD = false>
+template <typename T, int VEC, int SUB, int P, int PD, bool NT>
 __global__ __launch_bounds__(64 * P) void latency_split_kernel(T* __restrict__ buf, StepArgs a) {
     static_assert(SUB % 3 == 0, "rows are processed in groups of three");
     using V = Vec<T, VEC>;
     constexpr int G = SUB / 3;
     __shared__ V halo[P][2][64];
 
-    const uint32_t wg = a.wg_base + (XCD ? xcd_contiguous(blockIdx.x, gridDim.x) : blockIdx.x);
+    const uint32_t wg = a.wg_base + blockIdx.x;
     const uint32_t cb = wg % (uint32_t)a.colblocks;
     const uint32_t rest = wg / (uint32_t)a.colblocks;
     const int cyc = (int)(rest % (uint32_t)a.ncycles);
@@ -837,23 +837,28 @@ inline void set_columns(StepArgs* a, Launch* L, int cols) {
 // workgroups at most; the latency tiles use this to cap how many cycles a CU streams at once.
 constexpr size_t kLdsPerCu = 160 * 1024;
 
-// Resident workgroups per CU for each latency tile (0: no cap), measured best on MI355X over the
-// 81- and 243-rings, 27x27 and 9x9x9 at 8 MiB per rank. Fewer concurrent cycles keep fewer rows
+// Resident workgroups per CU for each latency tile (0: no cap), measured best on MI355X over
+// rings of 81 to 2187 ranks and 2D to 4D tori. Fewer concurrent cycles keep fewer rows
 // streaming at once; tiles whose waves walk many rows keep enough bytes in flight with one
 // workgroup per CU, while the 27-row tile (3 rows per wave) needs the full occupancy.
 template <int SUB, int P>
 constexpr int latency_wg_per_cu() {
-    return (SUB == 3 && P == 1) ? 16 : (SUB == 3 && P == 3) ? 4 : (SUB == 3 && P == 9) ? 0 : 1;
+    return (SUB == 3 && P == 1) ? 16
+         : (SUB == 3 && P == 3) ? 4
+         : (SUB == 9 && P == 1) ? 4
+         : (SUB == 3 && P == 9) ? 0
+                                : 1;
 }
 
-template <typename T, int VEC, int SUB, int P, bool XCD = false>
+template <typename T, int VEC, int SUB, int P>
 hipError_t launch_split(T* buf, StepArgs a, Launch L, hipStream_t stream) {
     set_columns(&a, &L, 64);
     constexpr int cap = latency_wg_per_cu<SUB, P>();
     constexpr size_t halo = (size_t)P * 2 * 64 * sizeof(Vec<T, VEC>);  // the kernel's own LDS
     constexpr size_t extra = cap ? kLdsPerCu / cap - halo - 256 : 0;   // unused, caps occupancy
-    return dispatch(latency_split_kernel<T, VEC, SUB, P, 1, true, XCD>, L.grid, 64 * P, stream,
-                    buf, a, extra);
+    static_assert(extra + halo <= kLdsPerCu, "a workgroup must fit in one CU's LDS");
+    return dispatch(latency_split_kernel<T, VEC, SUB, P, 1, true>, L.grid, 64 * P, stream, buf,
+                    a, extra);
 }
 
 template <typename T, int VEC>
@@ -863,13 +868,13 @@ hipError_t launch_latency(T* buf, const StepArgs& a, const Launch& L, int len,
         // rows per wavefront x wavefronts per workgroup, measured best on MI355X
         case 3: return launch_split<T, VEC, 3, 1>(buf, a, L, stream);
         case 9:
-            // the XCD-contiguous workgroup order measured 4-13% faster for 9-row cycles on tori
-            // of three or more dimensions, and 1.5-9% slower on rings
-            if (a.D >= 3) return launch_split<T, VEC, 3, 3, true>(buf, a, L, stream);
+            // one wave per cycle measured 5-10% faster on tori of three or more dimensions, and
+            // up to 2% slower on rings
+            if (a.D >= 3) return launch_split<T, VEC, 9, 1>(buf, a, L, stream);
             return launch_split<T, VEC, 3, 3>(buf, a, L, stream);
         case 27: return launch_split<T, VEC, 3, 9>(buf, a, L, stream);
         case 81: return launch_split<T, VEC, 9, 9>(buf, a, L, stream);
-        case 243: return launch_split<T, VEC, 27, 9>(buf, a, L, stream);
+        case 243: return launch_split<T, VEC, 81, 3>(buf, a, L, stream);
         // 81 rows per wavefront keep the register window in registers (72 VGPRs); 243 would spill
         case 729: return launch_split<T, VEC, 81, 9>(buf, a, L, stream);
         default: {

@@ -49,14 +49,14 @@ class _Limit:
         T.trivance_set_dispatch_limit(self.prev)
 
 
-# every launch path: latency steps with 3-, 9- (plain and XCD-ordered), 27-, 81- and 243-rank
-# cycles and the generic cycle kernel (729); block steps; tree steps on rings and tori, with the
-# short and the long offset table. The 10 x 10 x 10 torus takes 65,536 work-items per dispatch
+# every launch path: latency steps with 3-, 9- (three waves per cycle on rings, one on tori of
+# three or more dimensions), 27-, 81-, 243- and 729-rank cycles and the generic cycle kernel
+# (2187); block steps; tree steps on rings and tori, with the short and the long offset table. The 10 x 10 x 10 torus takes 65,536 work-items per dispatch
 # (about 500 dispatches per pass), the others 1024.
 CASES = [
     ((3,), "L", 64 * 3 * 40 + 4), ((9,), "L", 64 * 9 * 6 + 8), ((9, 9, 9), "L", 64 * 27 + 12),
     ((27,), "L", 64 * 27 * 3 + 4), ((81,), "L", 64 * 81 * 2 + 8), ((243,), "L", 64 * 243 + 4),
-    ((729,), "L", 2003), ((27,), "B", 64 * 27 * 6 + 4), ((9, 9), "B", 64 * 81 * 2 * 3 + 12),
+    ((729,), "L", 2003), ((2187,), "L", 333), ((27,), "B", 64 * 27 * 6 + 4), ((9, 9), "B", 64 * 81 * 2 * 3 + 12),
     ((8,), "B", 8 * 256 * 3 + 4), ((50,), "B", 7777), ((4, 8), "B", 64 * 32 * 2 * 3 + 12),
     ((4, 4, 4), "B", 64 * 64 * 3 + 20), ((10, 10, 10), "B", 3001),
 ]

@@ -48,6 +48,7 @@ SHAPES = [
     # rectangular tori (unequal sides; rotation reading in include/trivance.h)
     ((3, 9), 64 * 27 * 3 + 4), ((9, 3), 777), ((3, 27), 64 * 81 * 2 + 12),
     ((27, 3), 64 * 81 + 8), ((3, 3, 9), 64 * 81 * 2 + 4), ((9, 27), 64 * 243 + 4),
+    ((3, 9, 9), 64 * 243 + 4),
 ]
 
 
@@ -71,6 +72,24 @@ def test_parity_small(shape, dtype, variant):
         V = rng.integers(-(2 ** 31), 2 ** 31 - 1, size=(n, E), dtype=np.int32)
     got = run_hip(V, dims, variant)
     assert_matches_oracle(got, V, dims, variant, what=f"{dims} E={E} {dtype} {variant}")
+    if dtype == "i32":
+        np.testing.assert_array_equal(got, np.broadcast_to(allreduce.exact_int_sum(V), got.shape))
+
+
+# Latency-optimal only (the bandwidth-optimal oracle takes minutes at this many ranks): 9-row
+# cycles in each of four dimensions, one wave per cycle.
+@pytest.mark.parametrize("dtype", ["f32", "i32"])
+def test_parity_latency_4d_torus(dtype):
+    dims, E = (9, 9, 9, 9), 64 * 4 + 45
+    n = 6561
+    rng = np.random.default_rng(94 + E)
+    _say(f"[parity] dims={dims} E={E} dtype={dtype} variant=L")
+    if dtype == "f32":
+        V = rng.standard_normal((n, E), dtype=np.float32)
+    else:
+        V = rng.integers(-(2 ** 31), 2 ** 31 - 1, size=(n, E), dtype=np.int32)
+    got = run_hip(V, dims, "L")
+    assert_matches_oracle(got, V, dims, "L", what=f"{dims} E={E} {dtype} L")
     if dtype == "i32":
         np.testing.assert_array_equal(got, np.broadcast_to(allreduce.exact_int_sum(V), got.shape))
 
