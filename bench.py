@@ -40,30 +40,30 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # source it was measured on (sha256 of the source file, first 16 hex digits).
 MEASURED_TRAFFIC = {
     # profiles/<kernel>_<workload>.md
-    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "efca26cfa1b94003",
-        "bytes_per_launch": 1359214600},
-    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
-        "bytes_per_launch": 3248090325},
-    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
-        "bytes_per_launch": 1017890817},
-    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
-        "bytes_per_launch": 32569524620},
-    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
-        "bytes_per_launch": 251705451},
-    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
-        "bytes_per_launch": 283162324},
-    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
-        "bytes_per_launch": 2286967203},
-    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
-        "bytes_per_launch": 1550526050},
-    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
-        "bytes_per_launch": 9724115763},
-    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
-        "bytes_per_launch": 3248094362},
-    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
-        "bytes_per_launch": 1017897280},
-    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {"src_sha": "efca26cfa1b94003",
-        "bytes_per_launch": 32569529737},
+    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "b988dc10190d5444",
+        "bytes_per_launch": 1359205153},
+    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
+        "bytes_per_launch": 3248096367},
+    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
+        "bytes_per_launch": 1017893591},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
+        "bytes_per_launch": 32569712411},
+    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
+        "bytes_per_launch": 251703723},
+    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
+        "bytes_per_launch": 283160640},
+    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
+        "bytes_per_launch": 2286956352},
+    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
+        "bytes_per_launch": 1550522058},
+    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
+        "bytes_per_launch": 9724132178},
+    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
+        "bytes_per_launch": 3248099157},
+    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
+        "bytes_per_launch": 1017898583},
+    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
+        "bytes_per_launch": 32569714181},
 }
 
 
