@@ -831,9 +831,11 @@ inline void set_columns(StepArgs* a, Launch* L, int cols) {
     L->grid = (uint32_t)((int64_t)L->ncoll * a->ncycles * a->colblocks);
 }
 
-// LDS of one MI355X compute unit. A workgroup that asks for 1/k of it leaves room for k
-// workgroups at most; the latency tiles use this to cap how many cycles a CU streams at once.
+// LDS of one MI355X compute unit. A workgroup that asks for 1/k of it, less kLdsSlack bytes
+// (so that allocation rounding never leaves room for fewer than k), fits k times at most; the
+// latency tiles and the block reduce-scatter use this to cap how many workgroups a CU runs.
 constexpr size_t kLdsPerCu = 160 * 1024;
+constexpr size_t kLdsSlack = 256;
 
 // Resident workgroups per CU for each latency tile (0: no cap), measured best on MI355X over
 // rings of 81 to 2187 ranks and 2D to 4D tori. Fewer concurrent cycles keep fewer rows
@@ -853,7 +855,7 @@ hipError_t launch_split(T* buf, StepArgs a, Launch L, hipStream_t stream) {
     set_columns(&a, &L, 64);
     constexpr int cap = latency_wg_per_cu<SUB, P>();
     constexpr size_t halo = (size_t)P * 2 * 64 * sizeof(Vec<T, VEC>);  // the kernel's own LDS
-    constexpr size_t extra = cap ? kLdsPerCu / cap - halo - 256 : 0;   // unused, caps occupancy
+    constexpr size_t extra = cap ? kLdsPerCu / cap - halo - kLdsSlack : 0;  // unused: the cap
     static_assert(extra + halo <= kLdsPerCu, "a workgroup must fit in one CU's LDS");
     return dispatch(latency_split_kernel<T, VEC, SUB, P, 1, true>, L.grid, 64 * P, stream, buf,
                     a, extra);
@@ -896,7 +898,7 @@ hipError_t launch_block(T* buf, const StepArgs& a, const Launch& L, bool reduce,
     if (L.U != 1) return hipErrorInvalidValue;
     if (reduce)
         return dispatch(block_step_kernel<T, VEC, 1, true, true, true, 1>, a.total_units, 64,
-                        stream, buf, a, kLdsPerCu / kBlockRsWgPerCu - 256);
+                        stream, buf, a, kLdsPerCu / kBlockRsWgPerCu - kLdsSlack);
     return dispatch(block_step_kernel<T, VEC, 1, false, true, true, kWavesPerBlock>,
                     ((uint64_t)a.total_units + kWavesPerBlock - 1) / kWavesPerBlock, kBlockThreads,
                     stream, buf, a);
