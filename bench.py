@@ -40,30 +40,30 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # source it was measured on (sha256 of the source file, first 16 hex digits).
 MEASURED_TRAFFIC = {
     # profiles/<kernel>_<workload>.md
-    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "b988dc10190d5444",
-        "bytes_per_launch": 1359205153},
-    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
-        "bytes_per_launch": 3248096367},
-    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
-        "bytes_per_launch": 1017893591},
-    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
-        "bytes_per_launch": 32569712411},
-    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
-        "bytes_per_launch": 251703723},
-    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
-        "bytes_per_launch": 283160640},
-    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
-        "bytes_per_launch": 2286956352},
-    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
-        "bytes_per_launch": 1550522058},
-    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
-        "bytes_per_launch": 9724132178},
-    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
-        "bytes_per_launch": 3248099157},
-    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
-        "bytes_per_launch": 1017898583},
-    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {"src_sha": "b988dc10190d5444",
-        "bytes_per_launch": 32569714181},
+    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "b9e9a2e985792d8f",
+        "bytes_per_launch": 1359163899},
+    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
+        "bytes_per_launch": 3248091399},
+    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
+        "bytes_per_launch": 1017891776},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
+        "bytes_per_launch": 32569659862},
+    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
+        "bytes_per_launch": 251703463},
+    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
+        "bytes_per_launch": 283160366},
+    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
+        "bytes_per_launch": 2286952919},
+    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
+        "bytes_per_launch": 1550519861},
+    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
+        "bytes_per_launch": 9724180264},
+    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
+        "bytes_per_launch": 3248094300},
+    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
+        "bytes_per_launch": 1017897145},
+    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
+        "bytes_per_launch": 32569665793},
 }
 
 
