@@ -94,10 +94,12 @@ def test_parity_latency_4d_torus(dtype):
         np.testing.assert_array_equal(got, np.broadcast_to(allreduce.exact_int_sum(V), got.shape))
 
 
-@pytest.mark.parametrize("dims,variants", [((9,), "LB"), ((8,), "B"), ((4, 4), "B")])
+@pytest.mark.parametrize("dims,variants", [((9,), "LB"), ((8,), "B"), ((4, 4), "B"), ((81,), "L"),
+                                           ((243,), "L"), ((3, 9, 9), "LB")])
 def test_misaligned_rows_use_scalar_path(dims, variants):
     """A [n, E] view whose start is not 16-byte aligned still gives the oracle's result (block,
-    latency and tree steps)."""
+    latency and tree steps; latency tiles of 3-, 9-, 81- and 243-row cycles, with one and with
+    several waves per cycle)."""
     import paper_2602_17254_amd as T
 
     n = int(np.prod(dims))
