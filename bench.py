@@ -331,10 +331,42 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
     }
     del buf
     torch.cuda.empty_cache()
+    ceiling = copy_ceiling()
+    line["copy_ceiling"] = ceiling
+    roofline["vs_copy_ceiling"] = round(achieved / ceiling["GBps"], 4)
     if with_cpu:
         _say(f"[bench] {w.name}: CPU oracle on {len(cols)} columns")
         line["cpu_baseline"] = cpu_baseline(w, first_cols, cols, V_cols)
     return line
+
+
+def copy_ceiling(nbytes: int = 1 << 30, reps: int = 10) -> dict:
+    """The practical HBM ceiling in the same run: the library's plain streaming copy
+    (trivance_copy_device, one 16-byte non-temporal load and store per lane) of `nbytes`, timed
+    with HIP events on the stream it runs on. Bytes counted: read + written."""
+    import torch
+
+    import paper_2602_17254_amd as T
+
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1.0)
+    s = torch.cuda.current_stream()
+    for _ in range(3):
+        T.trivance_copy_device(dst, src, s)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    for _ in range(reps):
+        T.trivance_copy_device(dst, src, s)
+    e1.record(s)
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    gbps = 2 * nbytes / (ms * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"kernel": "copy_stream_kernel", "bytes_per_launch": 2 * nbytes,
+            "avg_launch_ms": round(ms, 4), "GBps": round(gbps, 1),
+            "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
 
 
 def copy_probe(nbytes: int, reps: int = 3) -> None:

@@ -246,6 +246,16 @@ int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topol
 int trivance_fill_hash_uniform(void* buffers, int n, int64_t elems, uint64_t seed, void* stream);
 
 /*
+ * trivance_copy_device -- benchmark helper (not part of the AllReduce): copies `bytes` bytes from
+ * device memory `src` to device memory `dst` with a plain streaming kernel (one 16-byte
+ * non-temporal load and store per lane, one-wave workgroups), the simplest kernel with the step
+ * kernels' access granularity. Its rate is the practical HBM ceiling reported beside them.
+ * Asynchronous on stream. EINVAL unless bytes >= 0, bytes % 16 == 0, both pointers are 16-byte
+ * aligned and the two ranges do not overlap; bytes == 0 does nothing.
+ */
+int trivance_copy_device(void* dst, const void* src, int64_t bytes, void* stream);
+
+/*
  * trivance_set_dispatch_limit -- the most work-items one kernel dispatch may hold (process-wide;
  * default and maximum 2^31, minimum 1024). A dispatch carries its grid size as a 32-bit count of
  * work-items, so every launch of this library whose grid is larger is issued as consecutive

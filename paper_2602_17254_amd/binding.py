@@ -75,6 +75,7 @@ def _lib():
         "trivance_congestion": (i64, [P, ctypes.POINTER(Topology), ctypes.POINTER(i64), i64]),
         "trivance_congestion_device": (ctypes.c_int, [P, ctypes.POINTER(Topology), P, i64, P]),
         "trivance_fill_hash_uniform": (ctypes.c_int, [P, ctypes.c_int, i64, ctypes.c_uint64, P]),
+        "trivance_copy_device": (ctypes.c_int, [P, P, i64, P]),
         "trivance_set_dispatch_limit": (i64, [i64]),
         "trivance_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     }
@@ -94,7 +95,7 @@ def exported_symbols() -> list:
              "trivance_algorithmic_bytes", "trivance_pass_bytes", "trivance_allreduce_emulated",
              "trivance_allreduce_emulated_steps", "trivance_congestion",
              "trivance_congestion_device", "trivance_fill_hash_uniform",
-             "trivance_set_dispatch_limit", "trivance_strerror"]
+             "trivance_copy_device", "trivance_set_dispatch_limit", "trivance_strerror"]
     return [n for n in names if hasattr(lib, n)]
 
 
@@ -254,6 +255,22 @@ def trivance_fill_hash_uniform(buffers, seed: int, stream=None) -> None:
     _check(_lib().trivance_fill_hash_uniform(ctypes.c_void_p(buffers.data_ptr()),
                                              buffers.shape[0], buffers.shape[1], seed,
                                              _stream_ptr(stream)), "trivance_fill_hash_uniform")
+
+
+def trivance_copy_device(dst, src, stream=None) -> None:
+    """Benchmark helper: copy the contiguous CUDA tensor `src` into `dst` (the same number of
+    bytes, a multiple of 16) with the library's streaming copy kernel."""
+    import torch
+
+    for name, t in (("dst", dst), ("src", src)):
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous CUDA tensor")
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("dst and src must hold the same number of bytes")
+    _check(_lib().trivance_copy_device(ctypes.c_void_p(dst.data_ptr()),
+                                       ctypes.c_void_p(src.data_ptr()), nbytes,
+                                       _stream_ptr(stream)), "trivance_copy_device")
 
 
 def trivance_set_dispatch_limit(work_items: int) -> int:

@@ -1,4 +1,7 @@
-// Device-side input generator (not part of the AllReduce): counter-based U(-1, 1) fp32 values
+// Device-side helpers that are not part of the AllReduce: the benchmark's streaming copy, and
+// the input generator below.
+//
+// Input generator: counter-based U(-1, 1) fp32 values
 // from SplitMix64 (Steele, Lea, Flood, "Fast splittable pseudorandom number generators",
 // OOPSLA 2014). Value i of the rank-major array (i = r * elems + e) is the k-th output of a
 // SplitMix64 generator started at state 0, k = seed * 2^40 + i + 1: h = mix(k * golden_gamma);
@@ -27,8 +30,41 @@ __global__ __launch_bounds__(256) void fill_hash_uniform_kernel(float* __restric
     }
 }
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Plain streaming copy, one 16-byte vector per lane, non-temporal, one-wave workgroups: the
+// simplest kernel with the step kernels' access granularity, timed as the practical ceiling.
+__global__ __launch_bounds__(64) void copy_stream_kernel(const u32x4* __restrict__ src,
+                                                         u32x4* __restrict__ dst, uint64_t nvec,
+                                                         uint64_t wg_base) {
+    const uint64_t i = (wg_base + blockIdx.x) * 64 + threadIdx.x;
+    if (i < nvec) __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+}
+
 }  // namespace
 }  // namespace trivance
+
+extern "C" int trivance_copy_device(void* dst, const void* src, int64_t bytes, void* stream) {
+    if (bytes < 0 || bytes % 16 != 0) return TRIVANCE_EINVAL;
+    if (bytes == 0) return TRIVANCE_OK;
+    if (!dst || !src || reinterpret_cast<uintptr_t>(dst) % 16 != 0 ||
+        reinterpret_cast<uintptr_t>(src) % 16 != 0)
+        return TRIVANCE_EINVAL;
+    const uint64_t nvec = (uint64_t)bytes / 16;
+    const char* s = static_cast<const char*>(src);
+    char* d = static_cast<char*>(dst);
+    if (s < d + bytes && d < s + bytes) return TRIVANCE_EINVAL;  // overlapping ranges
+    hipError_t err = hipSuccess;
+    trivance::for_each_dispatch((nvec + 63) / 64, 64, [&](uint32_t first, uint32_t count) {
+        hipLaunchKernelGGL(trivance::copy_stream_kernel, dim3(count), dim3(64), 0,
+                           reinterpret_cast<hipStream_t>(stream),
+                           static_cast<const trivance::u32x4*>(src),
+                           static_cast<trivance::u32x4*>(dst), nvec, (uint64_t)first);
+        err = hipGetLastError();
+        return err == hipSuccess;
+    });
+    return err == hipSuccess ? TRIVANCE_OK : TRIVANCE_EHIP;
+}
 
 extern "C" int trivance_fill_hash_uniform(void* buffers, int n, int64_t elems, uint64_t seed,
                                           void* stream) {

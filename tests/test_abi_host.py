@@ -304,3 +304,20 @@ def test_plan_matches_oracle_on_seeded_random_shapes(dims):
     for t in range(S):
         assert T.trivance_pass_bytes(p, E, t) == rs[t] * 4
         assert T.trivance_pass_bytes(p, E, 2 * S - 1 - t) == ag[t] * 4
+
+
+def test_copy_helper_rejects_bad_arguments_before_any_launch():
+    """trivance_copy_device checks size, alignment and overlap on the host; a zero-byte copy is a
+    no-op. None of these cases reaches the GPU."""
+    lib = T.binding._lib()
+    P = ctypes.c_void_p
+    EINVAL = -1
+    assert lib.trivance_copy_device(P(4096), P(8192), 0, None) == 0
+    assert lib.trivance_copy_device(None, None, 0, None) == 0
+    assert lib.trivance_copy_device(P(4096), P(8192), -16, None) == EINVAL
+    assert lib.trivance_copy_device(P(4096), P(8192), 24, None) == EINVAL    # not a multiple of 16
+    assert lib.trivance_copy_device(P(4104), P(8192), 16, None) == EINVAL    # dst misaligned
+    assert lib.trivance_copy_device(P(4096), P(8200), 16, None) == EINVAL    # src misaligned
+    assert lib.trivance_copy_device(None, P(8192), 16, None) == EINVAL
+    assert lib.trivance_copy_device(P(4096), P(4096 + 32), 64, None) == EINVAL  # overlap
+    assert lib.trivance_copy_device(P(4096 + 32), P(4096), 64, None) == EINVAL  # overlap
