@@ -63,6 +63,11 @@ int main(void) {
     CHECK(trivance_set_dispatch_limit(1 << 20) == ((int64_t)1 << 31));
     CHECK(trivance_set_dispatch_limit(100) == TRIVANCE_EINVAL);
     CHECK(trivance_set_dispatch_limit((int64_t)1 << 31) == (1 << 20));
+    /* the copy helper checks its arguments before any launch; a zero-byte copy does nothing */
+    CHECK(trivance_copy_device(NULL, NULL, 0, NULL) == TRIVANCE_OK);
+    CHECK(trivance_copy_device((void*)4096, (const void*)8192, 24, NULL) == TRIVANCE_EINVAL);
+    CHECK(trivance_copy_device((void*)4104, (const void*)8192, 16, NULL) == TRIVANCE_EINVAL);
+    CHECK(trivance_copy_device((void*)4096, (const void*)4128, 64, NULL) == TRIVANCE_EINVAL);
     trivance_plan_destroy(NULL);
 
     if (failures == 0) printf("abi_host ok\n");
