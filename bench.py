@@ -40,30 +40,30 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # source it was measured on (sha256 of the source file, first 16 hex digits).
 MEASURED_TRAFFIC = {
     # profiles/<kernel>_<workload>.md
-    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "b9e9a2e985792d8f",
-        "bytes_per_launch": 1359163899},
-    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
-        "bytes_per_launch": 3248091399},
-    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
-        "bytes_per_launch": 1017891776},
-    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
-        "bytes_per_launch": 32569659862},
-    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
-        "bytes_per_launch": 251703463},
-    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
-        "bytes_per_launch": 283160366},
-    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
-        "bytes_per_launch": 2286952919},
-    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
-        "bytes_per_launch": 1550519861},
-    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
-        "bytes_per_launch": 9724180264},
-    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
-        "bytes_per_launch": 3248094300},
-    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
-        "bytes_per_launch": 1017897145},
-    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {"src_sha": "b9e9a2e985792d8f",
-        "bytes_per_launch": 32569665793},
+    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "a788f015396fac01",
+        "bytes_per_launch": 1359169888},
+    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
+        "bytes_per_launch": 3248091467},
+    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
+        "bytes_per_launch": 1017891728},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
+        "bytes_per_launch": 32569532382},
+    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
+        "bytes_per_launch": 251703483},
+    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
+        "bytes_per_launch": 283160224},
+    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
+        "bytes_per_launch": 2286956084},
+    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
+        "bytes_per_launch": 1550517906},
+    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
+        "bytes_per_launch": 9724117915},
+    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
+        "bytes_per_launch": 3248094104},
+    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
+        "bytes_per_launch": 1017897153},
+    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
+        "bytes_per_launch": 32569664182},
 }
 
 

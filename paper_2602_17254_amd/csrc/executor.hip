@@ -988,11 +988,12 @@ int run_tree_impl(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t s
     a.f_cpb = make_fastdiv32((uint32_t)a.cpb);
     // Units per wave, measured on MI355X over rings and 2- to 4-dimensional tori. When blocks
     // fill less than 80% of their chunks on average (blocks of a few granules, e.g. 16 x 16 x 16
-    // ranks at 8 and 16 MiB, 32 x 32 at 1 MiB) the all-gather (one load per unit) takes eight,
-    // and the reduce-scatter two on rings and 2D tori; everything else takes one.
+    // ranks at 8 and 16 MiB, 32 x 32 at 1 MiB) the all-gather (one load per unit) takes eight on
+    // rings and 2D tori and two on tori of three or more dimensions, and the reduce-scatter two
+    // on rings and 2D tori; everything else takes one.
     const double fill = (double)elems / ((double)p->D * p->n * a.cpb * chunk);
     const int u_rs = fill < 0.8 && p->D <= 2 ? 2 : 1;
-    const int u_ag = fill < 0.8 ? 8 : 1;
+    const int u_ag = fill < 0.8 ? (p->D <= 2 ? 8 : 2) : 1;
     for (int pi = pb; pi < pe; ++pi) {
         const Pass& ps = p->passes[pi];
         int used = 0;
