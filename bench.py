@@ -132,10 +132,9 @@ def cpu_baseline(w, gpu_first_result_cols, cols, V_cols, seconds_target=10.0, ma
             np.broadcast_to(allreduce.exact_int_sum(V_cols), gpu_first_result_cols.shape)))}
     else:
         # the GPU's fp32 result on the sample against the fp64 sum: largest |error| / bound, where
-        # the bound is 4 S 2^-23 sum|v| (S = steps); below 1 means within the bound
-        S = T.trivance_plan(w.dims, w.variant).num_steps
+        # the bound is 4 ceil(log3 n) 2^-23 sum|v|; below 1 means within the bound
         err = np.abs(gpu_first_result_cols.astype(np.float64) - allreduce.fp64_sum(V_cols)[None, :])
-        bound = np.maximum(allreduce.fp32_error_bound(V_cols, S)[None, :], 1e-300)
+        bound = np.maximum(allreduce.fp32_error_bound(V_cols)[None, :], 1e-300)
         exact = {"gpu_fp64_bound_ratio_on_sample": round(float((err / bound).max()), 4)}
     import torch
 

@@ -135,14 +135,18 @@ int trivance_plan_num_passes(const trivance_plan_t* plan);
 /*
  * trivance_plan_step -- introspection of one pass for one collective.
  *   phase    <- a trivance_phase
- *   step     <- global step index t (all-gather passes run t = S-1 .. 0)
  *   dim      <- torus dimension used by this collective in this pass
  *   distance <- peer distance of this collective in this pass (3^(t div D) for equal sides; the
  *               tree step's distance for a side that is not a power of three)
  * Any output pointer may be NULL. EINVAL if pass or collective is out of range.
  */
 int trivance_plan_step(const trivance_plan_t* plan, int pass, int collective, int* phase,
-                       int* step, int* dim, int* distance);
+                       int* dim, int* distance);
+
+/* Global step index t (Sec. 5, Appendix B: t = d + D k) that pass `pass` materialises: 0 .. S-1
+ * for the latency-optimal and reduce-scatter passes, S-1 .. 0 for the all-gather passes (Sec. 4.1
+ * reverse order). Returns t >= 0, or EINVAL for a NULL plan or a pass out of range. */
+int trivance_plan_step_index(const trivance_plan_t* plan, int pass);
 
 /*
  * trivance_block_range -- element range [begin, end) of block `block` in segment `collective`
@@ -256,15 +260,17 @@ int trivance_fill_hash_uniform(void* buffers, int n, int64_t elems, uint64_t see
 int trivance_copy_device(void* dst, const void* src, int64_t bytes, void* stream);
 
 /*
- * trivance_set_dispatch_limit -- the most work-items one kernel dispatch may hold (process-wide;
- * default and maximum 2^31, minimum 1024). A dispatch carries its grid size as a 32-bit count of
- * work-items, so every launch of this library whose grid is larger is issued as consecutive
- * dispatches of whole workgroups on the same stream (the results do not depend on the split).
- * A smaller limit only adds dispatches; it exists to exercise the split at small sizes. Set it
- * while no call of this library is being enqueued. Returns the previous limit, or EINVAL for a
- * value outside [1024, 2^31].
+ * trivance_plan_with_dispatch_limit -- a new, independent plan equal to `plan` except that every
+ * launch made with it is issued as dispatches of at most `work_items` work-items (the default and
+ * maximum is 2^31). A dispatch carries its grid size as a 32-bit count of work-items, so every
+ * launch of this library whose grid is larger is issued as consecutive dispatches of whole
+ * workgroups on the same stream; the results do not depend on the split. A smaller limit only
+ * adds dispatches: it exists to exercise the split at small sizes. `plan` is not modified and
+ * stays valid; release `*out` with trivance_plan_destroy.
+ * Errors: EINVAL for a NULL plan or out, or work_items outside [1024, 2^31]; ENOMEM.
  */
-int64_t trivance_set_dispatch_limit(int64_t work_items);
+int trivance_plan_with_dispatch_limit(const trivance_plan_t* plan, int64_t work_items,
+                                      trivance_plan_t** out);
 
 /* Static description of a status code. */
 const char* trivance_strerror(int status);

@@ -208,9 +208,22 @@ def abs_sum(V: np.ndarray) -> np.ndarray:
     return np.abs(V.astype(np.float64)).sum(axis=0)
 
 
-def fp32_error_bound(V: np.ndarray, steps: int) -> np.ndarray:
-    """Per-column bound 4 * S * 2^-23 * sum_u |v_u| on |fp32 result - exact sum|.
+def ceil_log3(n: int) -> int:
+    """Smallest s with 3^s >= n: the step count of Theorem 1 and Sec. 4.4 on a ring of n."""
+    s, p = 0, 1
+    while p < n:
+        p *= 3
+        s += 1
+    return s
 
-    Each input passes through at most 2 S float additions (two per ternary joint reduction), so
-    the classical summation bound gives about 2 S * 2^-24 * sum |v|; the factor 4 is slack."""
-    return 4.0 * max(steps, 1) * 2.0 ** -23 * abs_sum(V)
+
+def fp32_error_bound(V: np.ndarray) -> np.ndarray:
+    """Per-column bound 4 * ceil(log3 n) * 2^-23 * sum_u |v_u| on |fp32 result - exact sum|, n the
+    number of ranks (rows of V).
+
+    Each input passes through at most two float additions per step (a ternary joint reduction),
+    so the classical summation bound is about 2 S * 2^-24 * sum |v| = S * 2^-23 * sum |v| for S
+    steps. S is ceil(log3 n) on rings and on tori whose sides are powers of three; a torus with
+    other sides can take a few more steps than that (32x32: 8 against 7), which the factor 4
+    covers."""
+    return 4.0 * max(ceil_log3(V.shape[0]), 1) * 2.0 ** -23 * abs_sum(V)

@@ -64,7 +64,9 @@ def _lib():
         "trivance_plan_num_steps": (ctypes.c_int, [P]),
         "trivance_plan_num_passes": (ctypes.c_int, [P]),
         "trivance_plan_step": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int] +
-                               [ctypes.POINTER(ctypes.c_int)] * 4),
+                               [ctypes.POINTER(ctypes.c_int)] * 3),
+        "trivance_plan_step_index": (ctypes.c_int, [P, ctypes.c_int]),
+        "trivance_plan_with_dispatch_limit": (ctypes.c_int, [P, i64, ctypes.POINTER(P)]),
         "trivance_block_range": (ctypes.c_int, [P, i64, ctypes.c_int, ctypes.c_int,
                                                 ctypes.POINTER(i64), ctypes.POINTER(i64)]),
         "trivance_algorithmic_bytes": (i64, [P, i64, ctypes.c_int]),
@@ -76,7 +78,6 @@ def _lib():
         "trivance_congestion_device": (ctypes.c_int, [P, ctypes.POINTER(Topology), P, i64, P]),
         "trivance_fill_hash_uniform": (ctypes.c_int, [P, ctypes.c_int, i64, ctypes.c_uint64, P]),
         "trivance_copy_device": (ctypes.c_int, [P, P, i64, P]),
-        "trivance_set_dispatch_limit": (i64, [i64]),
         "trivance_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     }
     for name, (res, args) in sig.items():
@@ -91,11 +92,12 @@ def exported_symbols() -> list:
     """Names the binding resolves (all of include/trivance.h)."""
     lib = ctypes.CDLL(LIB_PATH)
     names = ["trivance_plan", "trivance_plan_ex", "trivance_plan_destroy", "trivance_plan_num_steps",
-             "trivance_plan_num_passes", "trivance_plan_step", "trivance_block_range",
+             "trivance_plan_num_passes", "trivance_plan_step", "trivance_plan_step_index",
+             "trivance_plan_with_dispatch_limit", "trivance_block_range",
              "trivance_algorithmic_bytes", "trivance_pass_bytes", "trivance_allreduce_emulated",
              "trivance_allreduce_emulated_steps", "trivance_congestion",
              "trivance_congestion_device", "trivance_fill_hash_uniform",
-             "trivance_copy_device", "trivance_set_dispatch_limit", "trivance_strerror"]
+             "trivance_copy_device", "trivance_strerror"]
     return [n for n in names if hasattr(lib, n)]
 
 
@@ -147,11 +149,26 @@ def trivance_plan(dims, variant="L", placement="natural") -> Plan:
 
 
 def trivance_plan_step(plan: Plan, pass_index: int, collective: int = 0) -> tuple:
-    """(phase, step, dim, distance) of one pass for one collective."""
-    out = [ctypes.c_int() for _ in range(4)]
+    """(phase, dim, distance) of one pass for one collective."""
+    out = [ctypes.c_int() for _ in range(3)]
     _check(_lib().trivance_plan_step(plan.handle, pass_index, collective,
                                      *[ctypes.byref(o) for o in out]), "trivance_plan_step")
     return tuple(o.value for o in out)
+
+
+def trivance_plan_step_index(plan: Plan, pass_index: int) -> int:
+    """Global step index t that a pass materialises (all-gather passes run t = S-1 .. 0)."""
+    return _check(_lib().trivance_plan_step_index(plan.handle, pass_index),
+                  "trivance_plan_step_index")
+
+
+def trivance_plan_with_dispatch_limit(plan: Plan, work_items: int) -> Plan:
+    """A new plan equal to `plan` whose launches are issued as dispatches of at most `work_items`
+    work-items (1024 .. 2^31); `plan` itself is unchanged."""
+    h = ctypes.c_void_p()
+    _check(_lib().trivance_plan_with_dispatch_limit(plan.handle, int(work_items), ctypes.byref(h)),
+           "trivance_plan_with_dispatch_limit")
+    return Plan(h, plan.dims, plan.variant, plan.placement)
 
 
 def trivance_block_range(plan: Plan, elems: int, collective: int, block: int) -> tuple:
@@ -271,9 +288,3 @@ def trivance_copy_device(dst, src, stream=None) -> None:
     _check(_lib().trivance_copy_device(ctypes.c_void_p(dst.data_ptr()),
                                        ctypes.c_void_p(src.data_ptr()), nbytes,
                                        _stream_ptr(stream)), "trivance_copy_device")
-
-
-def trivance_set_dispatch_limit(work_items: int) -> int:
-    """Set the most work-items one kernel dispatch may hold (1024 .. 2^31); returns the previous
-    limit. Larger grids are issued as consecutive dispatches on the same stream."""
-    return _check(_lib().trivance_set_dispatch_limit(int(work_items)), "trivance_set_dispatch_limit")

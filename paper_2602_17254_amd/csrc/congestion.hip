@@ -211,7 +211,8 @@ int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topol
     const int64_t grid = (int64_t)P * plan->D * a.max_lines;
     if (grid >= ((int64_t)1 << 31)) return TRIVANCE_EUNSUPPORTED;
     const size_t lds = (size_t)(2 * max_side + 4) * sizeof(int);
-    const bool ok = trivance::for_each_dispatch((uint64_t)grid, 64, [&](uint32_t first, uint32_t count) {
+    const bool ok = trivance::for_each_dispatch((uint64_t)grid, 64, plan->dispatch_items,
+                                                [&](uint32_t first, uint32_t count) {
         a.wg_base = first;
         hipLaunchKernelGGL(trivance::congestion_kernel, dim3(count), dim3(64), lds,
                            reinterpret_cast<hipStream_t>(stream), loads_dev, a);

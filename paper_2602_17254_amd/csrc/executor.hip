@@ -712,15 +712,22 @@ __global__ __launch_bounds__(64) void tree_step_kernel(T* __restrict__ buf, Tree
 // ---------------------------------------------------------------------------------------------
 // Host side.
 
+// Where and how a call's launches go: the stream, and the most work-items of one dispatch (the
+// plan's limit).
+struct Exec {
+    hipStream_t stream;
+    int64_t items;
+};
+
 // Enqueues `kernel` over `grid` workgroups of `threads` work-items as consecutive dispatches of
 // whole workgroups (for_each_dispatch), each with its first workgroup in the argument block.
 template <typename T, typename Args>
-hipError_t dispatch(void (*kernel)(T*, Args), uint64_t grid, int threads, hipStream_t stream,
+hipError_t dispatch(void (*kernel)(T*, Args), uint64_t grid, int threads, const Exec& x,
                     T* buf, Args a, size_t dynamic_lds = 0) {
     hipError_t err = hipSuccess;
-    for_each_dispatch(grid, threads, [&](uint32_t first, uint32_t count) {
+    for_each_dispatch(grid, threads, x.items, [&](uint32_t first, uint32_t count) {
         a.wg_base = first;
-        hipLaunchKernelGGL(kernel, dim3(count), dim3(threads), dynamic_lds, stream, buf, a);
+        hipLaunchKernelGGL(kernel, dim3(count), dim3(threads), dynamic_lds, x.stream, buf, a);
         err = hipGetLastError();
         return err == hipSuccess;
     });
@@ -851,37 +858,36 @@ constexpr int latency_wg_per_cu() {
 }
 
 template <typename T, int VEC, int SUB, int P>
-hipError_t launch_split(T* buf, StepArgs a, Launch L, hipStream_t stream) {
+hipError_t launch_split(T* buf, StepArgs a, Launch L, const Exec& x) {
     set_columns(&a, &L, 64);
     constexpr int cap = latency_wg_per_cu<SUB, P>();
     constexpr size_t halo = (size_t)P * 2 * 64 * sizeof(Vec<T, VEC>);  // the kernel's own LDS
     constexpr size_t extra = cap ? kLdsPerCu / cap - halo - kLdsSlack : 0;  // unused: the cap
     static_assert(extra + halo <= kLdsPerCu, "a workgroup must fit in one CU's LDS");
-    return dispatch(latency_split_kernel<T, VEC, SUB, P, 1, true>, L.grid, 64 * P, stream, buf,
-                    a, extra);
+    return dispatch(latency_split_kernel<T, VEC, SUB, P, 1, true>, L.grid, 64 * P, x, buf, a,
+                    extra);
 }
 
 template <typename T, int VEC>
-hipError_t launch_latency(T* buf, const StepArgs& a, const Launch& L, int len,
-                          hipStream_t stream) {
+hipError_t launch_latency(T* buf, const StepArgs& a, const Launch& L, int len, const Exec& x) {
     switch (len) {
         // rows per wavefront x wavefronts per workgroup, measured best on MI355X
-        case 3: return launch_split<T, VEC, 3, 1>(buf, a, L, stream);
+        case 3: return launch_split<T, VEC, 3, 1>(buf, a, L, x);
         case 9:
             // one wave per cycle measured 5-10% faster on tori of three or more dimensions, and
             // up to 2% slower on rings
-            if (a.D >= 3) return launch_split<T, VEC, 9, 1>(buf, a, L, stream);
-            return launch_split<T, VEC, 3, 3>(buf, a, L, stream);
-        case 27: return launch_split<T, VEC, 3, 9>(buf, a, L, stream);
-        case 81: return launch_split<T, VEC, 9, 9>(buf, a, L, stream);
-        case 243: return launch_split<T, VEC, 81, 3>(buf, a, L, stream);
+            if (a.D >= 3) return launch_split<T, VEC, 9, 1>(buf, a, L, x);
+            return launch_split<T, VEC, 3, 3>(buf, a, L, x);
+        case 27: return launch_split<T, VEC, 3, 9>(buf, a, L, x);
+        case 81: return launch_split<T, VEC, 9, 9>(buf, a, L, x);
+        case 243: return launch_split<T, VEC, 81, 3>(buf, a, L, x);
         // 81 rows per wavefront keep the register window in registers (72 VGPRs); 243 would spill
-        case 729: return launch_split<T, VEC, 81, 9>(buf, a, L, stream);
+        case 729: return launch_split<T, VEC, 81, 9>(buf, a, L, x);
         default: {
             StepArgs b = a;
             Launch M = L;
             set_columns(&b, &M, kBlockThreads);
-            return dispatch(latency_step_kernel<T, VEC, 1>, M.grid, kBlockThreads, stream, buf, b);
+            return dispatch(latency_step_kernel<T, VEC, 1>, M.grid, kBlockThreads, x, buf, b);
         }
     }
 }
@@ -893,20 +899,20 @@ hipError_t launch_latency(T* buf, const StepArgs& a, const Launch& L, int len,
 constexpr int kBlockRsWgPerCu = 20;
 
 template <typename T, int VEC>
-hipError_t launch_block(T* buf, const StepArgs& a, const Launch& L, bool reduce,
-                        hipStream_t stream) {
+hipError_t launch_block(T* buf, const StepArgs& a, const Launch& L, bool reduce, const Exec& x) {
     if (L.U != 1) return hipErrorInvalidValue;
     if (reduce)
-        return dispatch(block_step_kernel<T, VEC, 1, true, true, true, 1>, a.total_units, 64,
-                        stream, buf, a, kLdsPerCu / kBlockRsWgPerCu - kLdsSlack);
+        return dispatch(block_step_kernel<T, VEC, 1, true, true, true, 1>, a.total_units, 64, x,
+                        buf, a, kLdsPerCu / kBlockRsWgPerCu - kLdsSlack);
     return dispatch(block_step_kernel<T, VEC, 1, false, true, true, kWavesPerBlock>,
                     ((uint64_t)a.total_units + kWavesPerBlock - 1) / kWavesPerBlock, kBlockThreads,
-                    stream, buf, a);
+                    x, buf, a);
 }
 
 template <typename T, int VEC>
 int run_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
                    int pe) {
+    const Exec x{stream, p->dispatch_items};
     StepArgs a;
     int64_t max_blk;
     int rc = base_args(p, elems, &a, &max_blk);
@@ -929,12 +935,11 @@ int run_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t 
                 a.c_first = c0;
                 a.ncycles = (p->n / side) * ps.distance[c0];
                 L.ncoll = same ? p->D : 1;
-                err = launch_latency<T, VEC>(buf, a, L, side / ps.distance[c0], stream);
+                err = launch_latency<T, VEC>(buf, a, L, side / ps.distance[c0], x);
             }
             a.c_first = 0;
         } else {
-            err = launch_block<T, VEC>(buf, a, L, ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER,
-                                       stream);
+            err = launch_block<T, VEC>(buf, a, L, ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER, x);
         }
         if (err != hipSuccess) return TRIVANCE_EHIP;
     }
@@ -942,11 +947,10 @@ int run_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t 
 }
 
 template <typename T, int VEC, int U, int DM, int CAP>
-hipError_t launch_tree(T* buf, const TreeArgs<DM, CAP>& a, bool rs, int64_t total,
-                       hipStream_t stream) {
+hipError_t launch_tree(T* buf, const TreeArgs<DM, CAP>& a, bool rs, int64_t total, const Exec& x) {
     const uint64_t waves = (uint64_t)((total + U - 1) / U);  // one wave per workgroup
-    if (rs) return dispatch(tree_step_kernel<T, VEC, U, true, DM, CAP>, waves, 64, stream, buf, a);
-    return dispatch(tree_step_kernel<T, VEC, U, false, DM, CAP>, waves, 64, stream, buf, a);
+    if (rs) return dispatch(tree_step_kernel<T, VEC, U, true, DM, CAP>, waves, 64, x, buf, a);
+    return dispatch(tree_step_kernel<T, VEC, U, false, DM, CAP>, waves, 64, x, buf, a);
 }
 
 // Offset-table entries of pass `pi` (all collectives).
@@ -963,6 +967,7 @@ size_t tree_entries(const trivance_plan_t* p, int pi) {
 template <typename T, int VEC, int DM, int CAP>
 int run_tree_impl(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
                   int pe) {
+    const Exec x{stream, p->dispatch_items};
     TreeArgs<DM, CAP> a;
     std::memset(&a, 0, sizeof(a));
     a.elems = elems;
@@ -1029,9 +1034,9 @@ int run_tree_impl(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t s
         const bool rs = ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER;
         hipError_t err;
         switch (rs ? u_rs : u_ag) {
-            case 8: err = launch_tree<T, VEC, 8>(buf, a, rs, total, stream); break;
-            case 2: err = launch_tree<T, VEC, 2>(buf, a, rs, total, stream); break;
-            default: err = launch_tree<T, VEC, 1>(buf, a, rs, total, stream); break;
+            case 8: err = launch_tree<T, VEC, 8>(buf, a, rs, total, x); break;
+            case 2: err = launch_tree<T, VEC, 2>(buf, a, rs, total, x); break;
+            default: err = launch_tree<T, VEC, 1>(buf, a, rs, total, x); break;
         }
         if (err != hipSuccess) return TRIVANCE_EHIP;
     }

@@ -55,7 +55,8 @@ extern "C" int trivance_copy_device(void* dst, const void* src, int64_t bytes, v
     char* d = static_cast<char*>(dst);
     if (s < d + bytes && d < s + bytes) return TRIVANCE_EINVAL;  // overlapping ranges
     hipError_t err = hipSuccess;
-    trivance::for_each_dispatch((nvec + 63) / 64, 64, [&](uint32_t first, uint32_t count) {
+    trivance::for_each_dispatch((nvec + 63) / 64, 64, trivance::kMaxDispatchItems,
+                                [&](uint32_t first, uint32_t count) {
         hipLaunchKernelGGL(trivance::copy_stream_kernel, dim3(count), dim3(64), 0,
                            reinterpret_cast<hipStream_t>(stream),
                            static_cast<const trivance::u32x4*>(src),

@@ -10,7 +10,6 @@
 // forwarded to peer p at step k are p + sum_{i>k} e_i 3^i; equivalently the blocks a rank keeps
 // after step k are those congruent to it modulo 3^(k+1). On a torus that congruence holds per
 // dimension, with the exponent counting the steps taken so far in that dimension.
-#include <atomic>
 #include <cmath>
 #include <cstdlib>
 #include <new>
@@ -324,20 +323,9 @@ int64_t max_block_granules(const trivance_plan_t* p, int64_t elems) {
     return best;
 }
 
-namespace {
-std::atomic<int64_t> g_dispatch_work_items{(int64_t)1 << 31};
-}  // namespace
-
-int64_t dispatch_work_items() { return g_dispatch_work_items.load(std::memory_order_relaxed); }
-
 }  // namespace trivance
 
 extern "C" {
-
-int64_t trivance_set_dispatch_limit(int64_t work_items) {
-    if (work_items < 1024 || work_items > ((int64_t)1 << 31)) return TRIVANCE_EINVAL;
-    return trivance::g_dispatch_work_items.exchange(work_items, std::memory_order_relaxed);
-}
 
 int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance_plan_t** out) {
     return trivance_plan_ex(n, torus_dims, ndims, variant, 0u, out);
@@ -455,15 +443,36 @@ int trivance_plan_num_passes(const trivance_plan_t* plan) {
 }
 
 int trivance_plan_step(const trivance_plan_t* plan, int pass, int collective, int* phase,
-                       int* step, int* dim, int* distance) {
+                       int* dim, int* distance) {
     if (!plan || pass < 0 || pass >= (int)plan->passes.size() || collective < 0 ||
         collective >= plan->D)
         return TRIVANCE_EINVAL;
     const Pass& ps = plan->passes[pass];
     if (phase) *phase = ps.phase;
-    if (step) *step = ps.step;
     if (dim) *dim = ps.dim[collective];
     if (distance) *distance = ps.distance[collective];
+    return TRIVANCE_OK;
+}
+
+int trivance_plan_step_index(const trivance_plan_t* plan, int pass) {
+    if (!plan || pass < 0 || pass >= (int)plan->passes.size()) return TRIVANCE_EINVAL;
+    return plan->passes[pass].step;
+}
+
+int trivance_plan_with_dispatch_limit(const trivance_plan_t* plan, int64_t work_items,
+                                      trivance_plan_t** out) {
+    if (!out) return TRIVANCE_EINVAL;
+    *out = nullptr;
+    if (!plan || work_items < 1024 || work_items > trivance::kMaxDispatchItems)
+        return TRIVANCE_EINVAL;
+    trivance_plan_t* p = nullptr;
+    try {
+        p = new trivance_plan_t(*plan);
+    } catch (const std::bad_alloc&) {
+        return TRIVANCE_ENOMEM;
+    }
+    p->dispatch_items = work_items;
+    *out = p;
     return TRIVANCE_OK;
 }
 

@@ -69,6 +69,8 @@ struct trivance_plan {
     // TRIVANCE_PLACE_BY_SCHEDULE (equal power-of-three sides, bandwidth-optimal): block j of
     // segment c lies at position trivance::placed_position(p, c, j).
     bool placed = false;
+    // Most work-items one kernel dispatch may hold (trivance_plan_with_dispatch_limit).
+    int64_t dispatch_items = (int64_t)1 << 31;
 };
 
 namespace trivance {
@@ -105,17 +107,17 @@ inline uint32_t fastdiv32_host(uint32_t x, FastDiv32 f) {
     return (uint32_t)((((uint64_t)(x << 1) * f.mul) >> 32) >> f.shift);
 }
 
-// Work-items of one kernel dispatch, at most (trivance_set_dispatch_limit; 2^31 by default).
-int64_t dispatch_work_items();
+// Most work-items of one kernel dispatch (also the default of every plan).
+constexpr int64_t kMaxDispatchItems = (int64_t)1 << 31;
 
 // A dispatch packet holds its grid size as a 32-bit count of work-items, and a larger grid is not
 // rejected: it runs only part of the workgroups. Launches therefore go through this loop, which
 // splits a grid of `grid` workgroups of `threads` work-items into consecutive dispatches of at
-// most dispatch_work_items() work-items; one(first, count) enqueues workgroups
-// [first, first + count) and returns false on failure, which ends the loop.
+// most `items` work-items; one(first, count) enqueues workgroups [first, first + count) and
+// returns false on failure, which ends the loop.
 template <typename F>
-inline bool for_each_dispatch(uint64_t grid, int threads, F&& one) {
-    const uint64_t per = std::max<uint64_t>(1, (uint64_t)dispatch_work_items() / (uint64_t)threads);
+inline bool for_each_dispatch(uint64_t grid, int threads, int64_t items, F&& one) {
+    const uint64_t per = std::max<uint64_t>(1, (uint64_t)items / (uint64_t)threads);
     for (uint64_t first = 0; first < grid; first += per)
         if (!one((uint32_t)first, (uint32_t)std::min(per, grid - first))) return false;
     return true;

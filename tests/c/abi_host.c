@@ -21,11 +21,16 @@ int main(void) {
     CHECK(trivance_plan(729, dims, 2, TRIVANCE_BANDWIDTH_OPT, &p) == TRIVANCE_OK && p != NULL);
     CHECK(trivance_plan_num_steps(p) == 6);
     CHECK(trivance_plan_num_passes(p) == 12);
-    int phase, step, dim, distance;
-    CHECK(trivance_plan_step(p, 0, 1, &phase, &step, &dim, &distance) == TRIVANCE_OK);
-    CHECK(phase == TRIVANCE_PHASE_REDUCE_SCATTER && step == 0 && dim == 1 && distance == 1);
-    CHECK(trivance_plan_step(p, 11, 0, &phase, &step, &dim, &distance) == TRIVANCE_OK);
-    CHECK(phase == TRIVANCE_PHASE_ALLGATHER && step == 0 && dim == 0 && distance == 1);
+    int phase, dim, distance;
+    CHECK(trivance_plan_step(p, 0, 1, &phase, &dim, &distance) == TRIVANCE_OK);
+    CHECK(phase == TRIVANCE_PHASE_REDUCE_SCATTER && dim == 1 && distance == 1);
+    CHECK(trivance_plan_step_index(p, 0) == 0);
+    CHECK(trivance_plan_step(p, 4, 0, &phase, &dim, &distance) == TRIVANCE_OK);
+    CHECK(phase == TRIVANCE_PHASE_REDUCE_SCATTER && dim == 0 && distance == 9);
+    CHECK(trivance_plan_step(p, 11, 0, &phase, &dim, &distance) == TRIVANCE_OK);
+    CHECK(phase == TRIVANCE_PHASE_ALLGATHER && dim == 0 && distance == 1);
+    CHECK(trivance_plan_step_index(p, 11) == 0 && trivance_plan_step_index(p, 6) == 5);
+    CHECK(trivance_plan_step_index(p, 12) == TRIVANCE_EINVAL);
     /* 3.5 w E (n - 1) for the bandwidth-optimal variant */
     const int64_t E = 1048576;
     CHECK(2 * trivance_algorithmic_bytes(p, E, TRIVANCE_F32) == 7 * 4 * E * 728);
@@ -33,14 +38,14 @@ int main(void) {
     CHECK(trivance_block_range(p, E, 1, -1, &b, &e) == TRIVANCE_OK && b == E / 2 && e == E);
     CHECK(trivance_block_range(p, E, 0, 0, &b, &e) == TRIVANCE_OK && b == 0 && e == 704);
     CHECK(trivance_congestion(p, NULL, NULL, 0) == (int64_t)12 * 729 * 4);
-    CHECK(trivance_plan_step(p, 12, 0, &phase, &step, &dim, &distance) == TRIVANCE_EINVAL);
+    CHECK(trivance_plan_step(p, 12, 0, &phase, &dim, &distance) == TRIVANCE_EINVAL);
     trivance_plan_destroy(p);
 
     /* a ring whose size is not a power of three (Sec. 4.4): two steps at distances 1 and 3 */
     trivance_plan_t* q = NULL;
     CHECK(trivance_plan(8, NULL, 0, TRIVANCE_BANDWIDTH_OPT, &q) == TRIVANCE_OK);
     CHECK(trivance_plan_num_steps(q) == 2);
-    CHECK(trivance_plan_step(q, 1, 0, NULL, NULL, NULL, &distance) == TRIVANCE_OK && distance == 3);
+    CHECK(trivance_plan_step(q, 1, 0, NULL, NULL, &distance) == TRIVANCE_OK && distance == 3);
     trivance_plan_destroy(q);
 
     /* message-contiguous placement: on a 27-ring block 1 lies at position 9 (digits reversed) */
@@ -59,10 +64,14 @@ int main(void) {
     CHECK(trivance_plan(80, dims, 2, TRIVANCE_LATENCY_OPT, &r) == TRIVANCE_EINVAL);
     CHECK(trivance_allreduce_emulated(NULL, 9, 0, TRIVANCE_F32, NULL, NULL) == TRIVANCE_EINVAL);
     CHECK(strcmp(trivance_strerror(TRIVANCE_ESIZE), "output buffer too small") == 0);
-    /* the dispatch limit: default 2^31, range [1024, 2^31], returns the previous value */
-    CHECK(trivance_set_dispatch_limit(1 << 20) == ((int64_t)1 << 31));
-    CHECK(trivance_set_dispatch_limit(100) == TRIVANCE_EINVAL);
-    CHECK(trivance_set_dispatch_limit((int64_t)1 << 31) == (1 << 20));
+    /* a derived plan with a lower dispatch limit: range [1024, 2^31], the original untouched */
+    trivance_plan_t* lim = NULL;
+    CHECK(trivance_plan(9, NULL, 0, TRIVANCE_LATENCY_OPT, &r) == TRIVANCE_OK);
+    CHECK(trivance_plan_with_dispatch_limit(r, 1 << 20, &lim) == TRIVANCE_OK && lim != NULL);
+    CHECK(trivance_plan_num_passes(lim) == 2 && trivance_plan_num_passes(r) == 2);
+    trivance_plan_destroy(lim);
+    CHECK(trivance_plan_with_dispatch_limit(r, 100, &lim) == TRIVANCE_EINVAL && lim == NULL);
+    trivance_plan_destroy(r);
     /* the copy helper checks its arguments before any launch; a zero-byte copy does nothing */
     CHECK(trivance_copy_device(NULL, NULL, 0, NULL) == TRIVANCE_OK);
     CHECK(trivance_copy_device((void*)4096, (const void*)8192, 24, NULL) == TRIVANCE_EINVAL);

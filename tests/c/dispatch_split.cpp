@@ -18,10 +18,10 @@ static int failures = 0;
     } while (0)
 
 static void covers(uint64_t grid, int threads, int64_t limit) {
-    CHECK(trivance_set_dispatch_limit(limit) > 0);
     uint64_t next = 0, pieces = 0;
     bool whole = true;
-    const bool ok = trivance::for_each_dispatch(grid, threads, [&](uint32_t first, uint32_t count) {
+    const bool ok = trivance::for_each_dispatch(grid, threads, limit,
+                                                [&](uint32_t first, uint32_t count) {
         whole = whole && first == next && count >= 1 &&
                 (uint64_t)count * (uint64_t)threads <= (uint64_t)limit;
         next = (uint64_t)first + count;
@@ -36,13 +36,25 @@ static void covers(uint64_t grid, int threads, int64_t limit) {
 }
 
 int main() {
-    const int64_t def = (int64_t)1 << 31;
-    CHECK(trivance_set_dispatch_limit(4096) == def);  // the default
-    CHECK(trivance::dispatch_work_items() == 4096);
-    CHECK(trivance_set_dispatch_limit(1023) == TRIVANCE_EINVAL);
-    CHECK(trivance_set_dispatch_limit(def + 1) == TRIVANCE_EINVAL);
-    CHECK(trivance_set_dispatch_limit(0) == TRIVANCE_EINVAL);
-    CHECK(trivance::dispatch_work_items() == 4096);
+    const int64_t def = trivance::kMaxDispatchItems;
+    CHECK(def == ((int64_t)1 << 31));
+
+    // a plan carries its limit; a derived plan has its own and leaves the original untouched
+    trivance_plan_t* p = nullptr;
+    CHECK(trivance_plan(27, nullptr, 0, TRIVANCE_BANDWIDTH_OPT, &p) == TRIVANCE_OK);
+    CHECK(p->dispatch_items == def);
+    trivance_plan_t* q = nullptr;
+    CHECK(trivance_plan_with_dispatch_limit(p, 4096, &q) == TRIVANCE_OK && q != nullptr);
+    CHECK(q->dispatch_items == 4096 && p->dispatch_items == def);
+    CHECK(q->passes.size() == p->passes.size() && q->n == p->n && q->S == p->S);
+    trivance_plan_t* r = reinterpret_cast<trivance_plan_t*>(1);
+    CHECK(trivance_plan_with_dispatch_limit(p, 1023, &r) == TRIVANCE_EINVAL && r == nullptr);
+    CHECK(trivance_plan_with_dispatch_limit(p, def + 1, &r) == TRIVANCE_EINVAL);
+    CHECK(trivance_plan_with_dispatch_limit(nullptr, 4096, &r) == TRIVANCE_EINVAL);
+    CHECK(trivance_plan_with_dispatch_limit(p, 4096, nullptr) == TRIVANCE_EINVAL);
+    trivance_plan_destroy(p);
+    CHECK(q->dispatch_items == 4096);  // still valid after the original is gone
+    trivance_plan_destroy(q);
 
     // a 3^18-wave grid of 256-thread workgroups (2.5e10 work-items) at the default limit
     covers(96855123, 256, def);
@@ -55,13 +67,11 @@ int main() {
     covers(12345, 256, 4096);
 
     // a failing dispatch ends the loop
-    CHECK(trivance_set_dispatch_limit(1024) > 0);
     int calls = 0;
-    const bool ok = trivance::for_each_dispatch(100, 256, [&](uint32_t, uint32_t) {
+    const bool ok = trivance::for_each_dispatch(100, 256, 1024, [&](uint32_t, uint32_t) {
         return ++calls < 3;
     });
     CHECK(!ok && calls == 3);
-    CHECK(trivance_set_dispatch_limit(def) == 1024);
 
     if (failures == 0) std::printf("dispatch_split ok\n");
     return failures == 0 ? 0 : 1;

@@ -50,7 +50,8 @@ def test_plan_matches_oracle_schedule(dims, variant):
         for c in range(t.D):
             got = T.trivance_plan_step(p, i, c)
             dim, dist = schedule.step_dim_and_distance(t, c, step)
-            assert got == (phase_code[ph], step, dim, dist)
+            assert got == (phase_code[ph], dim, dist)
+        assert T.trivance_plan_step_index(p, i) == step
 
 
 @pytest.mark.parametrize("E,dims", [(0, (9,)), (1, (9,)), (1000, (27,)), (64 * 243 * 3 + 17, (243,)),
@@ -136,17 +137,21 @@ def test_placement_is_rejected_where_it_does_not_apply():
     lib.trivance_plan_destroy(h)
 
 
-def test_dispatch_limit_range_and_previous_value():
-    prev = T.trivance_set_dispatch_limit(4096)
-    try:
-        assert prev == 2 ** 31
-        for bad in (0, -1, 1023, 2 ** 31 + 1):
-            with pytest.raises(T.TrivanceError):
-                T.trivance_set_dispatch_limit(bad)
-        assert T.trivance_set_dispatch_limit(1024) == 4096
-    finally:
-        T.trivance_set_dispatch_limit(prev)
-    assert T.trivance_set_dispatch_limit(2 ** 31) == 2 ** 31
+def test_dispatch_limit_is_a_derived_plan():
+    """The dispatch limit lives in a plan: a derived plan carries the lower limit and the same
+    schedule, the original is unchanged, and limits outside [1024, 2^31] are rejected."""
+    p = T.trivance_plan((27, 27), "B")
+    q = T.trivance_plan_with_dispatch_limit(p, 4096)
+    assert q.num_passes == p.num_passes and q.num_steps == p.num_steps
+    for i in range(p.num_passes):
+        for c in range(2):
+            assert T.trivance_plan_step(q, i, c) == T.trivance_plan_step(p, i, c)
+    for bad in (0, -1, 1023, 2 ** 31 + 1):
+        with pytest.raises(T.TrivanceError):
+            T.trivance_plan_with_dispatch_limit(p, bad)
+    assert T.trivance_plan_with_dispatch_limit(p, 2 ** 31).num_passes == p.num_passes
+    del p  # the derived plan stays usable
+    assert T.trivance_algorithmic_bytes(q, 1000) > 0
 
 
 def test_congestion_length_query_and_size_check():
@@ -187,7 +192,8 @@ def test_nonpower3_ring_plan_matches_oracle_tree(n):
     assert p.num_steps == S and p.num_passes == 2 * S
     E = 1000
     for i in range(2 * S):
-        phase, step, dim, d = T.trivance_plan_step(p, i)
+        phase, dim, d = T.trivance_plan_step(p, i)
+        step = T.trivance_plan_step_index(p, i)
         assert (phase, step, dim, d) == ((1 if i < S else 2), i if i < S else 2 * S - 1 - i, 0,
                                           dist[i if i < S else 2 * S - 1 - i])
     # oracle tree: receivers (parent offsets) and children per step, from the contribution paths
@@ -227,7 +233,8 @@ def test_nonpower3_torus_plan_matches_oracle(dims):
     for i in range(2 * S):
         t = i if i < S else 2 * S - 1 - i
         for c in range(D):
-            phase, step, dim, d = T.trivance_plan_step(p, i, c)
+            phase, dim, d = T.trivance_plan_step(p, i, c)
+            step = T.trivance_plan_step_index(p, i)
             want_dim, k = rot[c][t]
             assert (phase, step, dim, d) == ((1 if i < S else 2), t, want_dim,
                                               nonpow3.distances(dims[want_dim])[k])
@@ -287,7 +294,8 @@ def test_plan_matches_oracle_on_seeded_random_shapes(dims):
     rot = [nonpow3.torus_rotation(dims, c) for c in range(D)]
     for t in range(S):
         for c in range(D):
-            _, step, dim, d = T.trivance_plan_step(p, t, c)
+            _, dim, d = T.trivance_plan_step(p, t, c)
+            step = T.trivance_plan_step_index(p, t)
             assert (step, dim, d) == (t, rot[c][t][0], nonpow3.distances(dims[rot[c][t][0]])[rot[c][t][1]])
     bounds = partition.block_bounds(E, D, n)
     rs = [0] * S

@@ -1,8 +1,8 @@
 """GPU: launches issued as several dispatches.
 
 A dispatch carries its grid size as a 32-bit count of work-items; every launch of the library
-goes through a split into dispatches of at most trivance_set_dispatch_limit() work-items. Here a
-limit of 1024 work-items (one to sixteen workgroups per dispatch) forces the split on small
+goes through a split into dispatches of at most the plan's limit (2^31 work-items, lowered on a
+derived plan by trivance_plan_with_dispatch_limit). Here a limit of 1024 work-items (one to sixteen workgroups per dispatch) forces the split on small
 inputs for every kernel family, against the oracle; and a bandwidth-optimal call whose first
 pass holds 3^18 waves (2.5e10 work-items) runs at the default limit, against exact column sums.
 """
@@ -32,21 +32,6 @@ def _gpu_present():
 
     T.binding._lib()  # fails loudly when the native library is missing
     yield
-
-
-class _Limit:
-    def __init__(self, items):
-        self.items = items
-
-    def __enter__(self):
-        import paper_2602_17254_amd as T
-
-        self.prev = T.trivance_set_dispatch_limit(self.items)
-
-    def __exit__(self, *exc):
-        import paper_2602_17254_amd as T
-
-        T.trivance_set_dispatch_limit(self.prev)
 
 
 # every launch path: latency steps with 3-, 9- (three waves per cycle on rings, one on tori of
@@ -79,8 +64,7 @@ def test_split_dispatches_match_oracle(dims, variant, E, dtype):
         V = rng.standard_normal((n, E), dtype=np.float32)
     else:
         V = rng.integers(-(2 ** 31), 2 ** 31 - 1, size=(n, E), dtype=np.int32)
-    with _Limit(limit):
-        got = run_hip(V, dims, variant)
+    got = run_hip(V, dims, variant, dispatch_items=limit)
     assert_matches_oracle(got, V, dims, variant, what=f"split {dims} {variant} E={E} {dtype}")
     if dtype == "i32":
         np.testing.assert_array_equal(got, np.broadcast_to(allreduce.exact_int_sum(V), got.shape))
@@ -94,8 +78,7 @@ def test_split_dispatches_placed(dims, E):
     n = int(np.prod(dims))
     V = np.random.default_rng(n + E).integers(-(2 ** 31), 2 ** 31 - 1, size=(n, E), dtype=np.int32)
     _say(f"[split placed] dims={dims} E={E} limit=1024")
-    with _Limit(1024):
-        got = run_hip(V, dims, "B", placement="schedule")
+    got = run_hip(V, dims, "B", placement="schedule", dispatch_items=1024)
     seg, blk = placement_labels(E, dims)
     assert_matches_oracle(got, V, dims, "B", col_seg=seg, col_blk=blk, what=f"split placed {dims}")
 
@@ -106,8 +89,8 @@ def test_split_congestion_matches_oracle(dims, variant):
     import paper_2602_17254_amd as T
 
     _say(f"[split congestion] dims={dims} variant={variant} limit=1024")
-    with _Limit(1024):
-        got = T.trivance_congestion(T.trivance_plan(dims, variant))
+    plan = T.trivance_plan_with_dispatch_limit(T.trivance_plan(dims, variant), 1024)
+    got = T.trivance_congestion(plan)
     np.testing.assert_array_equal(got, congestion.link_loads(dims, variant))
 
 

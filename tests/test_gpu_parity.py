@@ -294,8 +294,8 @@ NONPOW3_TORI = [((4, 4), 64 * 16 * 2 * 3 + 4), ((2, 3), 101), ((8, 8), 64 * 64 *
                 ((10, 3, 3), 64 * 90 * 3 + 4), ((16, 16), 64 * 256 * 2 + 36), ((4, 4), 5),
                 ((8, 8), 0),
                 # blocks filling whole 256-element chunks: one unit per wave in both phases (the
-                # partly filled ones above take two (2D) or one (3D, 4D) in the reduce-scatter and
-                # eight in the all-gather)
+                # partly filled ones above take two units per wave (2D) or one (3D, 4D) in the
+                # reduce-scatter, and eight (2D) or two (3D, 4D) in the all-gather)
                 ((4, 4), 2 * 16 * 256 * 2), ((2, 3, 4), 3 * 24 * 256 + 12),
                 ((2, 2, 2), 3 * 8 * 4096 + 192), ((2, 2, 2, 2), 4 * 16 * 256 * 2),
                 # more than 64 offset-table entries per pass on 2D and 4D tori (the long table)

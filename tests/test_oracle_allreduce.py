@@ -52,13 +52,13 @@ def test_9x9x9_int32_small():
 @pytest.mark.parametrize("dims", [(9,), (27,), (81,), (3, 3), (9, 9), (3, 3, 3)])
 @pytest.mark.parametrize("variant", ["L", "B"])
 def test_fp32_within_summation_bound(dims, variant):
-    """(a): |fp32 - exact| <= 4 S 2^-23 sum|v| per column."""
+    """(a): |fp32 - exact| <= 4 ceil(log3 n) 2^-23 sum|v| per column."""
     rng = np.random.default_rng(11)
     t = schedule.Torus(dims)
     V = rng.standard_normal((t.n, 64 * t.n + 17), dtype=np.float32)
     out = allreduce.allreduce(V, dims, variant).astype(np.float64)
     err = np.abs(out - allreduce.fp64_sum(V)[None, :])
-    assert (err <= allreduce.fp32_error_bound(V, t.steps)[None, :]).all()
+    assert (err <= allreduce.fp32_error_bound(V)[None, :]).all()
 
 
 def test_n3_is_one_joint_reduction():
