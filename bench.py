@@ -3,16 +3,19 @@
 python bench.py [--steps K] [--warmup W] [--workload NAME | --all] [--no-cpu-baseline]
 
 A step is one whole emulated AllReduce (every pass of the schedule) over the workload's n rank
-vectors, which are resident in HBM before timing starts. K steps are timed back to back, bracketed
-by device synchronisation. Inside the timed region HIP events on the launch stream bracket each
-phase (all passes of the latency-optimal variant; the reduce-scatter and the all-gather), whose
+vectors, which are resident in HBM before timing starts. K steps are timed, bracketed by device
+synchronisation; before each, the inputs are restored on the device (outside the events), so
+every timed AllReduce works on the workload's own finite inputs. HIP events on the launch stream
+bracket each step and, inside it, each phase (all passes of the latency-optimal variant; the reduce-scatter and the all-gather), whose
 passes run back to back with one kernel family: group time / launches is that family's average
 launch duration, used for the roofline. One more step after the timed region brackets every pass
 with events (per-pass diagnostic only). Throughput counts the algorithmic
 bytes of the step-by-step schedule (each participating location read once and each output
 written once per pass; trivance_algorithmic_bytes).
 
-Default workload: 81 virtual ranks on a ring, latency-optimal variant, 8 MiB fp32 per rank.
+Default workload: the largest single-GPU configuration, a 9 x 9 x 9 torus (729 virtual ranks),
+bandwidth-optimal variant, 128 MiB of fp32 per rank (97.8 GB resident). Its line also summarises
+the other configurations of the metric, measured in the same run (`other_configs`).
 Prints one JSON line per workload.
 """
 
@@ -183,6 +186,75 @@ def _sample_for_baseline(w, budget_cols):
     return np.arange(start, start + budget_cols, dtype=np.int64)
 
 
+def _inputs_on_device(w, dtype, device_rng=False):
+    """The workload's inputs resident in HBM, and a function that restores them on a stream.
+
+    dtype 'f32' or 'i32' (the workload's int32 companion). The counter-based U(-1, 1) inputs are
+    regenerated in place on the device; host-generated inputs (numpy's N(0,1) and uniform int32,
+    the workload's recipe) are uploaded once into a pristine device copy and restored from it with
+    the library's streaming copy. With device_rng, N(0,1) and the int32 range come from torch's
+    seeded device generator instead (same distributions, other values; used by the summary of
+    the other configurations, which has no host-side oracle check).
+    Returns (buf, regen, V_host); V_host is None when the values exist only on the device."""
+    import torch
+
+    import paper_2602_17254_amd as T
+
+    shape = (w.n, w.elems)
+    if dtype == "f32" and w.dist == "hash_uniform":
+        buf = torch.empty(shape, dtype=torch.float32, device="cuda")
+        return buf, (lambda s: T.trivance_fill_hash_uniform(buf, w.seed, s)), None
+    V_host = None
+    if device_rng:
+        g = torch.Generator(device="cuda")
+        g.manual_seed(w.seed if dtype == "f32" else w.int_seed)
+        if dtype == "f32":
+            pristine = torch.randn(shape, dtype=torch.float32, device="cuda", generator=g)
+        else:
+            lo, hi = w.int_range
+            pristine = torch.randint(lo, hi + 1, shape, dtype=torch.int32, device="cuda",
+                                     generator=g)
+    else:
+        if dtype == "f32":
+            V_host = inputs.normal_f32(w.seed, w.n, w.elems)
+        else:
+            V_host = inputs.uniform_i32(w.int_seed, w.n, w.elems, *w.int_range)
+        pristine = torch.from_numpy(V_host).cuda()
+    buf = torch.empty_like(pristine)
+    return buf, (lambda s: T.trivance_copy_device(buf, pristine, s)), V_host
+
+
+def _all_finite(buf, rows=16):
+    """True if no element of the float tensor is inf or NaN (checked a few rows at a time)."""
+    import torch
+
+    return all(bool(torch.isfinite(buf[r:r + rows]).all()) for r in range(0, buf.shape[0], rows))
+
+
+def _timed_steps(buf, plan, regen, groups, steps, stream):
+    """K AllReduces; before each, the inputs are restored (outside the events). Returns the
+    per-step, per-phase-group event times (ms) and the wall time of the whole region (s)."""
+    import torch
+
+    import paper_2602_17254_amd as T
+
+    G = len(groups)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(G + 1)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        regen(stream)
+        ev[k][0].record(stream)
+        for g, (pb, pe, _) in enumerate(groups):
+            T.trivance_allreduce_emulated_steps(buf, plan, pb, pe, stream)
+            ev[k][g + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    group_ms = np.array([[ev[k][g].elapsed_time(ev[k][g + 1]) for g in range(G)]
+                         for k in range(steps)])
+    return group_ms, wall
+
+
 def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
     import torch
 
@@ -194,25 +266,13 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
     code = {"f32": T.F32, "i32": T.I32}[dtype]
     alg_bytes = T.trivance_algorithmic_bytes(plan, w.elems, code)
     pass_bytes = [T.trivance_pass_bytes(plan, w.elems, p, code) for p in range(P)]
+    if dtype == "i32" and w.int_range is None:
+        raise ValueError(f"{w.name} has no int32 input")
 
     # ---- inputs resident in HBM (untimed) ----
     _say(f"[bench] {w.name}: preparing inputs ({w.n} x {w.elems} {dtype})")
-    if dtype == "i32":
-        # the workload's int32 companion input: uniform integers in its stated range
-        if w.int_range is None:
-            raise ValueError(f"{w.name} has no int32 input")
-        buf = torch.empty((w.n, w.elems), dtype=torch.int32, device="cuda")
-        V_host = inputs.uniform_i32(w.int_seed, w.n, w.elems, *w.int_range)
-        buf.copy_(torch.from_numpy(V_host))
-    else:
-        buf = torch.empty((w.n, w.elems), dtype=torch.float32, device="cuda")
-        if w.dist == "hash_uniform":
-            T.trivance_fill_hash_uniform(buf, w.seed)
-            V_host = None
-        else:
-            V_host = inputs.normal_f32(w.seed, w.n, w.elems)
-            buf.copy_(torch.from_numpy(V_host))
-    torch.cuda.synchronize()
+    buf, regen, V_host = _inputs_on_device(w, dtype)
+    stream = torch.cuda.current_stream()
 
     # ---- first run: result kept for the CPU-baseline comparison ----
     # about 15 s of single-core oracle work: fewer columns as the rank count grows
@@ -223,42 +283,34 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
     else:
         V_cols = inputs.hash_uniform(w.seed, w.elems, np.arange(w.n), cols)
     del V_host
-    T.trivance_allreduce_emulated(buf, plan)
+    regen(stream)
+    T.trivance_allreduce_emulated(buf, plan, stream)
     torch.cuda.synchronize()
     first_cols = None
     if with_cpu:
         first_cols = buf.index_select(1, torch.from_numpy(cols).cuda()).cpu().numpy()
 
-    # ---- warmup ----
+    # ---- warmup (inputs restored before each AllReduce, like the timed steps) ----
     for _ in range(warmup):
-        T.trivance_allreduce_emulated(buf, plan)
+        regen(stream)
+        T.trivance_allreduce_emulated(buf, plan, stream)
     torch.cuda.synchronize()
 
     # Passes of one phase run back to back with one kernel family (latency: every pass; reduce-
     # scatter; all-gather), so events at the phase boundaries give each family's average launch
     # duration (group time / launches) without a timing marker between every two kernels.
     groups = phase_groups([T.trivance_plan_step(plan, p)[0] for p in range(P)])
-    G = len(groups)
 
-    # ---- timed region: K steps, events at the phase boundaries on the launch stream ----
-    stream = torch.cuda.current_stream()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(G + 1)] for _ in range(steps)]
+    # ---- timed region: K AllReduces on freshly restored inputs, events on the launch stream ----
     _say(f"[bench] {w.name}: timing {steps} steps x {P} passes")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(steps):
-        ev[k][0].record(stream)
-        for g, (pb, pe, _) in enumerate(groups):
-            T.trivance_allreduce_emulated_steps(buf, plan, pb, pe, stream)
-            ev[k][g + 1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    group_ms = np.array([[ev[k][g].elapsed_time(ev[k][g + 1]) for g in range(G)]
-                         for k in range(steps)])
-    ms_per_step = wall * 1e3 / steps
+    group_ms, wall = _timed_steps(buf, plan, regen, groups, steps, stream)
+    step_ms = group_ms.sum(axis=1)
+    ms_per_step = float(step_ms.mean())
     value = alg_bytes / (ms_per_step * 1e-3) / 1e9
+    finite = _all_finite(buf) if dtype == "f32" else True
 
     # ---- after the timed region: one diagnostic step with an event around every pass ----
+    regen(stream)
     pev = [torch.cuda.Event(enable_timing=True) for _ in range(P + 1)]
     for p in range(P):
         pev[p].record(stream)
@@ -294,6 +346,7 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
         "traffic": traffic,
         "alg_bytes_per_launch": int(dom_bytes),
         "avg_launch_ms": round(dom_ms, 4),
+        "launches_per_step": launches,
     }
     line = {
         "metric": METRIC,
@@ -316,19 +369,25 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
             "n_ranks": w.n,
             "elems_per_rank": w.elems,
             "rank_bytes": w.rank_bytes,
+            "resident_bytes": w.n * w.rank_bytes,
             "passes": P,
             "alg_bytes_per_step": alg_bytes,
             "input": w.dist if dtype == "f32" else f"uniform int32 {w.int_range}",
         },
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
-        "step_ms_events": {"median": round(float(np.median(group_ms.sum(axis=1))), 4),
-                           "min": round(float(group_ms.sum(axis=1).min()), 4),
-                           "max": round(float(group_ms.sum(axis=1).max()), 4)},
+        "timing": "ms_per_step = mean of the K event-timed AllReduces on the launch stream; the "
+                  "inputs are restored before every AllReduce, outside the events",
+        "step_ms_events": {"mean": round(ms_per_step, 4),
+                           "median": round(float(np.median(step_ms)), 4),
+                           "min": round(float(step_ms.min()), 4),
+                           "max": round(float(step_ms.max()), 4)},
+        "wall_ms_per_step_incl_input_restore": round(wall * 1e3 / steps, 4),
+        "timed_outputs_finite": finite,
         "per_pass_ms_diagnostic": [round(float(x), 4) for x in per_pass_ms],
         "roofline": roofline,
         "cpu_baseline": None,
     }
-    del buf
+    del buf, regen
     torch.cuda.empty_cache()
     ceiling = copy_ceiling()
     line["copy_ceiling"] = ceiling
@@ -337,6 +396,64 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
         _say(f"[bench] {w.name}: CPU oracle on {len(cols)} columns")
         line["cpu_baseline"] = cpu_baseline(w, first_cols, cols, V_cols)
     return line
+
+
+# The other named configurations of the metric, summarised inside the headline line.
+SUMMARY_JOBS = [("ring9_L_4KiB", "f32"), ("ring81_L_8MiB", "f32"), ("ring243_B_32MiB", "f32"),
+                ("ring243_B_32MiB", "i32"), ("torus27x27_B_4MiB", "f32")]
+
+
+def summary_line(w, dtype, steps=10, warmup=2):
+    """Throughput of one more configuration in the same run, with inputs from torch's seeded
+    device generator (the workload's distribution) restored before every timed AllReduce, and a
+    check of the result on the device: int32 against the exact column sums, fp32 within
+    4 ceil(log3 n) 2^-23 sum|v| of an fp64 sum."""
+    import torch
+
+    import paper_2602_17254_amd as T
+
+    plan = T.trivance_plan(w.dims, w.variant, w.placement)
+    code = {"f32": T.F32, "i32": T.I32}[dtype]
+    alg_bytes = T.trivance_algorithmic_bytes(plan, w.elems, code)
+    steps_bound = 0
+    while 3 ** steps_bound < w.n:  # ceil(log3 n)
+        steps_bound += 1
+    _say(f"[bench] summary {w.name} {dtype}")
+    buf, regen, _ = _inputs_on_device(w, dtype, device_rng=True)
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        regen(stream)
+        T.trivance_allreduce_emulated(buf, plan, stream)
+    groups = phase_groups([T.trivance_plan_step(plan, p)[0] for p in range(plan.num_passes)])
+    group_ms, _ = _timed_steps(buf, plan, regen, groups, steps, stream)
+    ms = float(group_ms.sum(axis=1).mean())
+    # result check on the last timed AllReduce: restore a copy of its inputs, compare column sums
+    # over every column, a few rows at a time
+    out = buf.clone()
+    regen(stream)
+    torch.cuda.synchronize()
+    ok = True
+    for e0 in range(0, w.elems, 1 << 20):
+        e1 = min(w.elems, e0 + (1 << 20))
+        if dtype == "i32":
+            exact = buf[:, e0:e1].to(torch.int64).sum(0)
+            exact = ((exact + 2 ** 31) % 2 ** 32 - 2 ** 31).to(torch.int32)
+            ok = ok and bool((out[:, e0:e1] == exact[None, :]).all())
+        else:
+            x = buf[:, e0:e1].to(torch.float64)
+            bound = 4.0 * steps_bound * 2.0 ** -23 * x.abs().sum(0)
+            err = (out[:, e0:e1].to(torch.float64) - x.sum(0)[None, :]).abs()
+            ok = ok and bool((err <= bound[None, :]).all())
+    del buf, regen, out
+    torch.cuda.empty_cache()
+    gbps = alg_bytes / (ms * 1e-3) / 1e9
+    return {"workload": w.name, "dtype": dtype, "ms_per_step": round(ms, 4),
+            "GBps": round(gbps, 1), "pct_of_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
+            "steps": steps, "input": "torch device generator, " +
+            ("N(0,1)" if dtype == "f32" else f"uniform int32 {w.int_range}"),
+            "result_check": ("exact column sums" if dtype == "i32" else
+                             "within 4 ceil(log3 n) 2^-23 sum|v| of fp64"),
+            "result_ok": ok}
 
 
 def copy_ceiling(nbytes: int = 1 << 30, reps: int = 10) -> dict:
@@ -440,6 +557,8 @@ def main():
     ap.add_argument("--workload", default=inputs.HEADLINE, choices=sorted(inputs.WORKLOADS))
     ap.add_argument("--all", action="store_true", help="every named workload, one line each")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-summary", action="store_true",
+                    help="skip the summary of the other configurations in the headline line")
     ap.add_argument("--dtype", default="f32", choices=["f32", "i32"],
                     help="element type (i32 needs a workload with an int32 input)")
     ap.add_argument("--sweep", action="store_true",
@@ -466,6 +585,8 @@ def main():
     for name, dtype in jobs:
         line = run_workload(inputs.WORKLOADS[name], args.steps, args.warmup,
                             with_cpu=not args.no_cpu_baseline, dtype=dtype)
+        if not args.all and not args.no_summary and name == inputs.HEADLINE:
+            line["other_configs"] = [summary_line(inputs.WORKLOADS[n], d) for n, d in SUMMARY_JOBS]
         print(json.dumps(line), flush=True)
 
 

@@ -124,5 +124,6 @@ WORKLOADS = {
     ]
 }
 
-# The headline single-GPU workload: 81 virtual ranks on a ring, latency-optimal, 8 MiB per rank.
-HEADLINE = "ring81_L_8MiB"
+# The headline single-GPU workload: the largest configuration of the metric's 8-128 MiB range, a
+# 9 x 9 x 9 torus of 729 virtual ranks, bandwidth-optimal, 128 MiB per rank (97.8 GB resident).
+HEADLINE = "torus9x9x9_B_128MiB"
