@@ -30,12 +30,62 @@ def test_n7_figure():
         assert (stats["blocks_sent"][k] == want).all()
 
 
-def test_n32_final_distance():
-    """Sec. 4.4: 27 of 32 blocks before the final step; the 5 missing ones come from both sides,
-    so the final distance is ceil(5 / 2) = 3."""
+def test_n32_reading_departs_from_the_27_of_32_count():
+    """Reading 13 on the 32-ring: the final distance is ceil((32 - 27) / 2) = 3 (Sec. 4.4), the
+    owner of a block holds 15 of the 32 contributions before the final step and receives 17 in
+    it, and every rank forwards every block exactly once (31 forwards per block and phase).
+
+    Sec. 4.4 counts 27 held before the final step and 5 arriving in it. That count is the reading
+    NOT taken: the ranks at +/-3 that send in the final step lie inside the owner's 27-window, so
+    holding the whole window before the final step would need them to forward the block twice,
+    against the paper's at-most-once bound (tests/test_nonpow3_trees.py proves this and shows by
+    enumeration that the reading holds as many contributions before the final step as any
+    single-forwarding tree can)."""
+    g = _golden()
     f, d = nonpow3.levels(32)
-    assert 3 ** f == _golden()["n32_blocks_before_final"]["value"]
-    assert d == math.ceil((32 - 27) / 2) == 3
+    assert d == math.ceil((32 - g["n32_blocks_before_final"]["value"]) / 2) == 3
+    # which contributions reach block 0's owner without the final step
+    S = len(nonpow3.distances(32))
+    held = {u for u in range(32) if nonpow3.position(32, u, 0, S - 1) == 0}
+    assert len(held) == 15 and len(held) != g["n32_blocks_before_final"]["value"]
+    arriving = {u for u in range(32) if nonpow3.position(32, u, 0, S - 1) in (3, 29)}
+    assert len(arriving) == 17 and held | arriving == set(range(32))
+    # one forward per block and rank: 31 forwards of each block over the phase
+    stats = {}
+    nonpow3.bandwidth_optimal_ring(np.zeros((32, 0), np.int32), stats=stats)
+    assert stats["blocks_sent"].sum() == 32 * 31
+    assert (stats["blocks_sent"].sum(axis=(0, 2)) == 31).all()
+
+
+def test_n7_and_n8_block0_trees_written_out():
+    """fp32 association of block 0 on the 7- and 8-rings, derived by hand from reading 13.
+
+    n = 7 (f = 1, window |o| <= 1, final distance 2): ranks 2 and 3 form the + tree (3 sends to 2
+    in step 0), ranks 5 and 4 the - tree (4 sends to 5); the owner first combines its neighbours,
+    then in the final step the partial from 5 (its left peer at distance 2) and the one from 2:
+        ((((v0 + v6) + v1) + (v5 + v4)) + (v2 + v3)).
+    n = 8 (final distance 3; the odd remainder puts the extra rank on the + side): ranks 2, 3, 4
+    form the + tree rooted at 3 (2 from its left, 4 from its right), ranks 6, 5 the - tree rooted
+    at 5 (6 sends from its right):
+        (((v0 + v7) + v1) + (v5 + v6)) + ((v3 + v2) + v4).
+    Each is a (own + left) + right joint reduction at every receiver (Sec. 4.3), absent terms
+    skipped. Inputs spanning twelve decades make other associations round differently."""
+    from oracle import partition
+
+    for n, tree in ((7, lambda v: (((v[0] + v[6]) + v[1]) + (v[5] + v[4])) + (v[2] + v[3])),
+                    (8, lambda v: (((v[0] + v[7]) + v[1]) + (v[5] + v[6])) + ((v[3] + v[2]) + v[4]))):
+        rng = np.random.default_rng(70 + n)
+        E = 64 * n * 4
+        V = (rng.standard_normal((n, E)) * np.logspace(-6, 6, E)).astype(np.float32)
+        want = tree(V)
+        out = nonpow3.bandwidth_optimal_ring(V)
+        _, blk = partition.column_labels(E, 1, n)
+        np.testing.assert_array_equal(out[0, blk == 0], want[blk == 0])
+        # the written-out order is observable: summing left to right gives other bits
+        naive = V[0].copy()
+        for u in range(1, n):
+            naive = naive + V[u]
+        assert not np.array_equal(naive[blk == 0], want[blk == 0])
 
 
 @pytest.mark.parametrize("n", range(2, 244))
