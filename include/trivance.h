@@ -241,6 +241,42 @@ int64_t trivance_congestion(const trivance_plan_t* plan, const trivance_topology
 int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topology* topo,
                                int64_t* loads_dev, int64_t loads_len, void* stream);
 
+/* Result of trivance_cost_model (all times in the units of alpha and beta). */
+typedef struct {
+    double total;        /* C(m, A) = latency + transmission                                     */
+    double latency;      /* passes x alpha                                                       */
+    double transmission; /* beta x the sum over passes of the busiest directed link's bytes      */
+    double theta;        /* that sum relative to m / D: the transmission-delay factor of Tables 1
+                            and 2 (relative to m on a ring)                                     */
+    int passes;          /* number of passes, i.e. steps(A)                                      */
+} trivance_cost_result;
+
+/*
+ * trivance_cost_model -- the congestion-aware cost model of Sec. 2.1 for this plan (host only,
+ * synchronous, no GPU work):
+ *     C(m, A) = steps(A) alpha + sum over passes of beta m_k c_k,
+ * where m_k c_k is read per directed link: the bytes of every message crossing the pass's busiest
+ * link. Every rank of a collective sends one message to each side along its active dimension over
+ * the pass's distance, so each directed link of that dimension carries `distance` of them per
+ * collective. Message sizes for m bytes per rank split into D segments of m / D and n blocks of
+ * m / (n D): the whole segment (latency-optimal, Sec. 4.2); n / 3^(t+1) blocks at step t of both
+ * phases (bandwidth-optimal, Sec. 4.1, Lemma 1); on sides that are not powers of three the blocks
+ * the tree forwards that way in the step (Sec. 4.4). Blocks are taken as exact fractions of m
+ * (the partition's 64-element rounding is not modelled). Trivance's distances are below half
+ * their side, so the scheduled direction is the shortest path (Appendix E).
+ *
+ *   bytes_per_rank   m, the AllReduce size per rank, in bytes (>= 0)
+ *   alpha            per-step start-up latency (e.g. seconds), >= 0
+ *   beta             transmission time per byte of one link (e.g. seconds per byte), >= 0
+ *   pass_link_bytes  optional host array [pass_len]: receives the busiest link's bytes per pass
+ *   out              receives the totals
+ * Errors: EINVAL for a NULL plan or out or a negative (or NaN) m, alpha or beta; ESIZE if
+ * pass_link_bytes is given and pass_len < the number of passes; EUNSUPPORTED for a Bruck plan.
+ */
+int trivance_cost_model(const trivance_plan_t* plan, double bytes_per_rank, double alpha,
+                        double beta, double* pass_link_bytes, int pass_len,
+                        trivance_cost_result* out);
+
 /*
  * trivance_fill_hash_uniform -- input generator (not part of the AllReduce): writes U(-1, 1)
  * fp32 values to the device array `buffers` of n * elems floats, value (r, e) being the k-th

@@ -35,6 +35,12 @@ class TrivanceError(RuntimeError):
         super().__init__(f"{what} failed: {_lib().trivance_strerror(status).decode()} ({status})")
 
 
+class CostResult(ctypes.Structure):
+    _fields_ = [("total", ctypes.c_double), ("latency", ctypes.c_double),
+                ("transmission", ctypes.c_double), ("theta", ctypes.c_double),
+                ("passes", ctypes.c_int)]
+
+
 class Topology(ctypes.Structure):
     _fields_ = [("ndims", ctypes.c_int), ("dims", ctypes.c_int * MAX_DIMS),
                 ("routing", ctypes.c_int)]
@@ -78,6 +84,9 @@ def _lib():
         "trivance_congestion_device": (ctypes.c_int, [P, ctypes.POINTER(Topology), P, i64, P]),
         "trivance_fill_hash_uniform": (ctypes.c_int, [P, ctypes.c_int, i64, ctypes.c_uint64, P]),
         "trivance_copy_device": (ctypes.c_int, [P, P, i64, P]),
+        "trivance_cost_model": (ctypes.c_int, [P, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                               ctypes.POINTER(ctypes.c_double), ctypes.c_int,
+                                               ctypes.POINTER(CostResult)]),
         "trivance_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     }
     for name, (res, args) in sig.items():
@@ -97,7 +106,7 @@ def exported_symbols() -> list:
              "trivance_algorithmic_bytes", "trivance_pass_bytes", "trivance_allreduce_emulated",
              "trivance_allreduce_emulated_steps", "trivance_congestion",
              "trivance_congestion_device", "trivance_fill_hash_uniform",
-             "trivance_copy_device", "trivance_strerror"]
+             "trivance_copy_device", "trivance_cost_model", "trivance_strerror"]
     return [n for n in names if hasattr(lib, n)]
 
 
@@ -288,3 +297,17 @@ def trivance_copy_device(dst, src, stream=None) -> None:
     _check(_lib().trivance_copy_device(ctypes.c_void_p(dst.data_ptr()),
                                        ctypes.c_void_p(src.data_ptr()), nbytes,
                                        _stream_ptr(stream)), "trivance_copy_device")
+
+
+def trivance_cost_model(plan: Plan, bytes_per_rank: float, alpha: float = 0.0,
+                        beta: float = 0.0) -> dict:
+    """The Sec. 2.1 cost model of the plan for an AllReduce of `bytes_per_rank` bytes per rank:
+    total, latency and transmission times, theta, passes, and the busiest link's bytes per
+    pass."""
+    P = plan.num_passes
+    peaks = (ctypes.c_double * max(P, 1))()
+    res = CostResult()
+    _check(_lib().trivance_cost_model(plan.handle, float(bytes_per_rank), float(alpha), float(beta),
+                                      peaks, max(P, 1), ctypes.byref(res)), "trivance_cost_model")
+    return {"total": res.total, "latency": res.latency, "transmission": res.transmission,
+            "theta": res.theta, "passes": res.passes, "pass_link_bytes": list(peaks)[:P]}

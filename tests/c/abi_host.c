@@ -39,6 +39,16 @@ int main(void) {
     CHECK(trivance_block_range(p, E, 0, 0, &b, &e) == TRIVANCE_OK && b == 0 && e == 704);
     CHECK(trivance_congestion(p, NULL, NULL, 0) == (int64_t)12 * 729 * 4);
     CHECK(trivance_plan_step(p, 12, 0, &phase, &dim, &distance) == TRIVANCE_EINVAL);
+    /* the Sec. 2.1 cost model: Table 2's 104/81 for 27 x 27, 12 alphas, per-pass link bytes */
+    {
+        trivance_cost_result cr;
+        double peaks[12];
+        CHECK(trivance_cost_model(p, 729.0 * 2.0, 1.5e-6, 1e-11, peaks, 12, &cr) == TRIVANCE_OK);
+        CHECK(cr.passes == 12 && cr.theta > 104.0 / 81.0 - 1e-12 && cr.theta < 104.0 / 81.0 + 1e-12);
+        CHECK(cr.latency > 12 * 1.5e-6 - 1e-18 && cr.latency < 12 * 1.5e-6 + 1e-18);
+        CHECK(peaks[0] > 243.0 - 1e-9 && peaks[0] < 243.0 + 1e-9); /* m / (D 3) */
+        CHECK(trivance_cost_model(p, 1.0, 0.0, 0.0, peaks, 11, &cr) == TRIVANCE_ESIZE);
+    }
     trivance_plan_destroy(p);
 
     /* a ring whose size is not a power of three (Sec. 4.4): two steps at distances 1 and 3 */
