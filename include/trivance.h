@@ -64,7 +64,8 @@ typedef enum {
     TRIVANCE_EUNSUPPORTED = -2,/* valid request outside what is implemented (see each call)    */
     TRIVANCE_EHIP = -3,        /* the HIP runtime reported an error (launch, copy, allocation) */
     TRIVANCE_ENOMEM = -4,      /* host memory allocation failed                                */
-    TRIVANCE_ESIZE = -5        /* caller-provided output is too small                          */
+    TRIVANCE_ESIZE = -5,       /* caller-provided output is too small                          */
+    TRIVANCE_ESCRATCH = -6     /* request larger than the library's fixed device scratch       */
 } trivance_status;
 
 /*
@@ -240,6 +241,20 @@ int64_t trivance_congestion(const trivance_plan_t* plan, const trivance_topology
  * `stream`; allocates nothing. */
 int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topology* topo,
                                int64_t* loads_dev, int64_t loads_len, void* stream);
+
+/*
+ * trivance_congestion_noalloc -- trivance_congestion for callers that cannot allocate device
+ * memory (serving loops and harnesses that forbid hipMalloc): the same host array, the same
+ * arguments, NULL loads returning the required length and ESIZE as there, but computed into a
+ * fixed device scratch that the library holds, one per GPU, from the first call on that GPU
+ * until the process ends. Calls no hipMalloc, hipFree or other allocating routine.
+ * Limit: at most 2^20 entries (passes x n x 2 D; 8 MiB of scratch); larger plans return
+ * TRIVANCE_ESCRATCH before any GPU work. Synchronous. Every call on one GPU uses that GPU's
+ * scratch, so calls that overlap on one GPU (from several host threads) race; calls on
+ * different GPUs do not. Errors: those of trivance_congestion, and ESCRATCH.
+ */
+int64_t trivance_congestion_noalloc(const trivance_plan_t* plan, const trivance_topology* topo,
+                                    int64_t* loads, int64_t loads_len);
 
 /* Result of trivance_cost_model (all times in the units of alpha and beta). */
 typedef struct {

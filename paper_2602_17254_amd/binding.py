@@ -82,6 +82,7 @@ def _lib():
                                                              P, P, ctypes.c_int, ctypes.c_int]),
         "trivance_congestion": (i64, [P, ctypes.POINTER(Topology), ctypes.POINTER(i64), i64]),
         "trivance_congestion_device": (ctypes.c_int, [P, ctypes.POINTER(Topology), P, i64, P]),
+        "trivance_congestion_noalloc": (i64, [P, ctypes.POINTER(Topology), ctypes.POINTER(i64), i64]),
         "trivance_fill_hash_uniform": (ctypes.c_int, [P, ctypes.c_int, i64, ctypes.c_uint64, P]),
         "trivance_copy_device": (ctypes.c_int, [P, P, i64, P]),
         "trivance_cost_model": (ctypes.c_int, [P, ctypes.c_double, ctypes.c_double, ctypes.c_double,
@@ -105,7 +106,7 @@ def exported_symbols() -> list:
              "trivance_plan_with_dispatch_limit", "trivance_block_range",
              "trivance_algorithmic_bytes", "trivance_pass_bytes", "trivance_allreduce_emulated",
              "trivance_allreduce_emulated_steps", "trivance_congestion",
-             "trivance_congestion_device", "trivance_fill_hash_uniform",
+             "trivance_congestion_device", "trivance_congestion_noalloc", "trivance_fill_hash_uniform",
              "trivance_copy_device", "trivance_cost_model", "trivance_strerror"]
     return [n for n in names if hasattr(lib, n)]
 
@@ -255,6 +256,20 @@ def trivance_congestion(plan: Plan, routing: str = "scheduled") -> np.ndarray:
     _check(lib.trivance_congestion(plan.handle, ctypes.byref(topo),
                                    out.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), need),
            "trivance_congestion")
+    return out.reshape(plan.num_passes, plan.n, 2 * plan.D)
+
+
+def trivance_congestion_noalloc(plan: Plan, routing: str = "scheduled") -> np.ndarray:
+    """trivance_congestion computed in the library's fixed device scratch (no device allocation;
+    at most 2^20 entries)."""
+    lib = _lib()
+    topo = _topology(plan, routing)
+    need = _check(lib.trivance_congestion_noalloc(plan.handle, ctypes.byref(topo), None, 0),
+                  "trivance_congestion_noalloc")
+    out = np.zeros(need, dtype=np.int64)
+    _check(lib.trivance_congestion_noalloc(plan.handle, ctypes.byref(topo),
+                                           out.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), need),
+           "trivance_congestion_noalloc")
     return out.reshape(plan.num_passes, plan.n, 2 * plan.D)
 
 

@@ -18,8 +18,17 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 
 #include "plan.h"
+
+// Device scratch of the allocation-free form, trivance_congestion_noalloc: the loads are computed
+// into it and copied to the caller's host array. Every GPU the library runs on holds its own copy
+// until the process ends. In host code `scratch` names a host-side stand-in, not device memory:
+// its device address is taken per device with hipGetSymbolAddress (scratch_address below) and only
+// that address is used.
+constexpr int64_t kScratchEntries = (int64_t)1 << 20;  // 8 MiB of int64 loads
+static __device__ __align__(256) int64_t scratch[kScratchEntries];
 
 namespace trivance {
 namespace {
@@ -152,6 +161,31 @@ __global__ __launch_bounds__(64) void congestion_kernel(int64_t* __restrict__ lo
 
 using trivance::CongArgs;
 
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+int64_t* g_scratch[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up once per device with that device
+// current.
+int scratch_address(int64_t** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return TRIVANCE_EHIP;
+    if (dev < 0 || dev >= kMaxDevices) return TRIVANCE_EUNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+            return TRIVANCE_EHIP;
+        g_scratch[dev] = static_cast<int64_t*>(ptr);
+    }
+    *out = g_scratch[dev];
+    return TRIVANCE_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topology* topo,
@@ -238,6 +272,25 @@ int64_t trivance_congestion(const trivance_plan_t* plan, const trivance_topology
     }
     if (hipFree(dev) != hipSuccess && rc == TRIVANCE_OK) rc = TRIVANCE_EHIP;
     return rc;
+}
+
+int64_t trivance_congestion_noalloc(const trivance_plan_t* plan, const trivance_topology* topo,
+                                    int64_t* loads, int64_t loads_len) {
+    if (!plan) return TRIVANCE_EINVAL;
+    const int64_t need = (int64_t)plan->passes.size() * plan->n * 2 * plan->D;
+    if (!loads) return need;
+    if (loads_len < need) return TRIVANCE_ESIZE;
+    if (need == 0) return TRIVANCE_OK;
+    if (need > kScratchEntries) return TRIVANCE_ESCRATCH;
+    int64_t* dev = nullptr;
+    int rc = scratch_address(&dev);
+    if (rc != TRIVANCE_OK) return rc;
+    // the kernel writes every entry of [0, need), so the scratch needs no clearing
+    rc = trivance_congestion_device(plan, topo, dev, need, nullptr);
+    if (rc != TRIVANCE_OK) return rc;
+    if (hipMemcpy(loads, dev, need * sizeof(int64_t), hipMemcpyDeviceToHost) != hipSuccess)
+        return TRIVANCE_EHIP;
+    return TRIVANCE_OK;
 }
 
 }  // extern "C"

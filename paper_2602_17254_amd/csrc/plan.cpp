@@ -543,6 +543,7 @@ const char* trivance_strerror(int status) {
         case TRIVANCE_EHIP: return "HIP runtime error";
         case TRIVANCE_ENOMEM: return "out of host memory";
         case TRIVANCE_ESIZE: return "output buffer too small";
+        case TRIVANCE_ESCRATCH: return "request exceeds the fixed device scratch";
         default: return "unknown status";
     }
 }
