@@ -20,6 +20,12 @@ congestion  hop-by-hop link-load walk (cost model of Sec. 2.1) and the transmiss
 nonpow3     rings and tori whose sides are not all powers of three (Sec. 4.4): the final-step
             distance, the reduction tree of every side, a mailbox emulation of the bandwidth-
             optimal variant and a column-by-column gather form of it, and their link loads.
+latency_nonpow3
+            the latency-optimal variant on sides that are not all powers of three: the partial
+            sums every rank keeps (windows, and the sub-window partials the final step of a side
+            needs), worked out backwards from the result, and the schedule run on them.
+cost        the congestion-aware cost model of Sec. 2.1 on the oracle's own messages, walked hop
+            by hop.
 placement   an optional block placement (not the default partition): block j at the position
             spelled by its base-3 digits in the order the schedule fixes them, which makes every
             kept set and message contiguous.
