@@ -86,20 +86,28 @@ typedef enum {
  * dimension, in cyclic order from (c + t) mod D, in which it still has steps left, at distance
  * 3^(steps it already took there). With equal sides both rules coincide.
  *
- * Sides that are not powers of three (Sec. 4.4; bandwidth-optimal variant only): a side of s with
- * 3^f < s < 3^(f+1) takes f steps at distances 3^0 .. 3^(f-1) and a final step at
- * ceil((s - 3^f) / 2), so ceil(log3 s) steps; S is the sum over the sides, and the dimension of
- * every step follows the rule for unequal sides above. The paper gives no construction of the
- * block sets; every block is reduced along one tree per dimension, built so that each rank
- * forwards each block once per phase (the tree of a side that is a power of three is the
- * ordinary one). Limits: at most 4 dimensions, sides up to 2200, at most 20 steps, and at most
- * 768 offset-table entries per step (the lists travel in kernel arguments).
+ * Sides that are not powers of three (Sec. 4.4): a side of s with 3^f < s < 3^(f+1) takes f steps
+ * at distances 3^0 .. 3^(f-1) and a final step at d = ceil((s - 3^f) / 2), so ceil(log3 s) steps;
+ * S is the sum over the sides, and the dimension of every step follows the rule for unequal sides
+ * above. The paper gives no construction of the block sets or partial sums:
+ *   - bandwidth-optimal: every block is reduced along one tree per dimension, built so that each
+ *     rank forwards each block once per phase (the tree of a side that is a power of three is the
+ *     ordinary one). Limits: at most 4 dimensions, sides up to 2200, at most 20 steps, and at
+ *     most 768 offset-table entries per step (the lists travel in kernel arguments).
+ *   - latency-optimal: a rank keeps its Lemma 2 window and, besides it, the partial sums over
+ *     parts of its window that a peer will need from it: in the final step along a side the
+ *     peer at +d sends the sum of the top d sources of its window and the peer at -d the sum of
+ *     the s - 3^f - d sources beyond the receiver's window on that side (offsets taken in
+ *     (-s/2, s/2], so an odd remainder puts the extra source on the + side); each such partial
+ *     is formed in earlier steps from the parts of it that lie in the three previous windows.
+ *     A rank holds at most 64 partials per collective between passes (more: EUNSUPPORTED); they
+ *     live in a caller-provided workspace (trivance_workspace_bytes,
+ *     trivance_allreduce_emulated_ws). Limits: at most 4 dimensions, sides up to 2200.
  *
  * Errors: EINVAL for out == NULL, n < 1, ndims < 0, a side < 1, product != n;
- *         EUNSUPPORTED for a side that is not a power of three with the latency-optimal or
- *         Bruck variant (the paper does not say how whole pre-reduced vectors would avoid
- *         counting the final step's overlap twice), beyond the limits above,
- *         ndims > TRIVANCE_MAX_DIMS, or TRIVANCE_BRUCK_REF on more than one dimension.
+ *         EUNSUPPORTED for a side that is not a power of three with the Bruck variant, beyond
+ *         the limits above, ndims > TRIVANCE_MAX_DIMS, or TRIVANCE_BRUCK_REF on more than one
+ *         dimension.
  */
 int trivance_plan(int n, const int* torus_dims, int ndims, int variant, trivance_plan_t** out);
 
@@ -166,7 +174,9 @@ int trivance_block_range(const trivance_plan_t* plan, int64_t elems, int collect
 /*
  * trivance_algorithmic_bytes -- bytes the step-by-step schedule must move through memory for one
  * AllReduce of `elems` elements per rank (each participating location read once and each output
- * written once per pass). Latency-optimal: 2 S n elems w. Bandwidth-optimal: reduce-scatter step t
+ * written once per pass). Latency-optimal: 2 S n elems w (with partial sums on sides that are not
+ * powers of three: every partial a rank holds before a pass read once, every one after it
+ * written once). Bandwidth-optimal: reduce-scatter step t
  * reads n elems w / 3^t and writes a third of that; all-gather step t reads n elems w / 3^(t+1)
  * and writes twice that; in total 3.5 w elems (n - 1) for divisible sizes (the exact sum over the
  * actual blocks is returned). Sides that are not powers of three: in every tree step each
@@ -202,8 +212,11 @@ int64_t trivance_pass_bytes(const trivance_plan_t* plan, int64_t elems, int dtyp
  * synchronisation happens, so the call can be captured into a HIP graph (replays reproduce it).
  * n == 1 or elems == 0 is a valid no-op. Calls that overlap on the same buffers race; calls on
  * different buffers may run concurrently on different streams.
+ * Plans whose trivance_workspace_bytes is not zero (latency-optimal with a side that is not a
+ * power of three) need trivance_allreduce_emulated_ws; this form returns ESIZE for them.
  * Errors: EINVAL (NULL plan/buffers with elems > 0, n mismatch, elems < 0, bad dtype),
- * EUNSUPPORTED (a Bruck plan, sizes beyond 32-bit work-unit counts), EHIP (launch failure).
+ * EUNSUPPORTED (a Bruck plan, sizes beyond 32-bit work-unit counts), ESIZE (a plan that needs a
+ * workspace), EHIP (launch failure).
  */
 int trivance_allreduce_emulated(void* buffers, int n, int64_t elems, int dtype,
                                 const trivance_plan_t* plan, void* stream);
@@ -214,6 +227,36 @@ int trivance_allreduce_emulated(void* buffers, int n, int64_t elems, int dtype,
 int trivance_allreduce_emulated_steps(void* buffers, int n, int64_t elems, int dtype,
                                       const trivance_plan_t* plan, void* stream, int pass_begin,
                                       int pass_end);
+
+/*
+ * trivance_workspace_bytes -- device workspace an AllReduce of `elems` elements per rank needs
+ * with this plan: 0 for every plan that runs in place (all bandwidth-optimal plans and the
+ * latency-optimal ones whose sides are powers of three). A latency-optimal plan with a side that
+ * is not a power of three keeps up to P partial sums per rank between passes (P = the plan's
+ * largest slot count) in two halves of P * n * elems values each (one when the plan has at most
+ * two steps): 4 bytes per value for both dtypes. Negative status on bad arguments.
+ */
+int64_t trivance_workspace_bytes(const trivance_plan_t* plan, int64_t elems, int dtype);
+
+/*
+ * trivance_allreduce_emulated_ws -- trivance_allreduce_emulated with a caller-owned device
+ * workspace of at least trivance_workspace_bytes(plan, elems, dtype) bytes (NULL with 0 bytes is
+ * fine for plans that need none). The workspace holds the partial sums between passes (Sec. 4.4,
+ * latency-optimal: see trivance_plan); its contents on entry do not matter and are left
+ * undefined. A 16-byte aligned workspace keeps the 16-byte vector path. Calls that share a
+ * workspace or buffers race. Errors: those of trivance_allreduce_emulated, and ESIZE for a
+ * workspace below the required size.
+ */
+int trivance_allreduce_emulated_ws(void* buffers, int n, int64_t elems, int dtype,
+                                   const trivance_plan_t* plan, void* workspace,
+                                   int64_t workspace_bytes, void* stream);
+
+/* Same, running only passes [pass_begin, pass_end). Consecutive ranges must use the same
+ * workspace: it carries the partial sums from one range to the next. */
+int trivance_allreduce_emulated_steps_ws(void* buffers, int n, int64_t elems, int dtype,
+                                         const trivance_plan_t* plan, void* workspace,
+                                         int64_t workspace_bytes, void* stream, int pass_begin,
+                                         int pass_end);
 
 /*
  * trivance_congestion -- per-pass, per-directed-link message counts (Sec. 2.1: c_k = number of

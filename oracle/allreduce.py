@@ -176,8 +176,12 @@ def bandwidth_optimal(V: np.ndarray, dims, col_seg=None, col_blk=None, rs_passes
 
 def allreduce(V: np.ndarray, dims, variant: str, **kw) -> np.ndarray:
     if nonpow3.is_tree(dims):
+        if variant == "L":
+            from . import latency_nonpow3
+
+            return latency_nonpow3.latency_optimal(V, dims, col_seg=kw.get("col_seg"))
         if variant != "B":
-            raise ValueError("sides that are not powers of three: bandwidth-optimal only")
+            raise ValueError(f"unknown variant {variant!r}")
         if len(dims) == 1:
             return nonpow3.bandwidth_optimal_ring(V, col_blk=kw.get("col_blk"))
         seg, blk = kw.get("col_seg"), kw.get("col_blk")

@@ -68,7 +68,38 @@ def passes_of(torus: schedule.Torus, variant: str) -> list:
     return schedule.pass_list(torus, variant)
 
 
+def _link_loads_latency_tree(dims, routing):
+    """Latency-optimal schedule on sides that are not all powers of three: a rank sends towards a
+    side in a pass when its peer there takes some partial from it (latency_nonpow3)."""
+    from . import latency_nonpow3
+
+    dims = tuple(int(x) for x in dims)
+    D = len(dims)
+    n = int(np.prod(dims))
+    S = sum(nonpow3.dim_steps(s) for s in dims)
+    loads = np.zeros((S, n, 2 * D), dtype=np.int64)
+    strides = np.cumprod((1,) + dims[:-1])
+    for c in range(D):
+        rot = nonpow3.torus_rotation(dims, c)
+        for t, ((dim, k), (plus, minus)) in enumerate(zip(rot, latency_nonpow3.message_slots(dims, c))):
+            dist = nonpow3.distances(dims[dim])[k]
+            for r in range(n):
+                for off, count in ((+dist, plus), (-dist, minus)):
+                    if not count:
+                        continue
+                    direction, hops = _route(off, dims[dim], routing)
+                    port = 2 * dim + (0 if direction > 0 else 1)
+                    node = r
+                    for _ in range(hops):
+                        loads[t, node, port] += 1
+                        x = (node // strides[dim]) % dims[dim]
+                        node += (((x + direction) % dims[dim]) - x) * strides[dim]
+    return loads
+
+
 def link_loads(dims, variant: str, routing: str = "scheduled") -> np.ndarray:
+    if variant == "L" and nonpow3.is_tree(dims):
+        return _link_loads_latency_tree(dims, routing)
     if variant == "B" and nonpow3.is_tree(dims):
         # Sec. 4.4 trees; every distance is below half its side, so both routings agree
         if len(dims) == 1:

@@ -16,6 +16,8 @@ but messages walked hop by hop:
   * sides that are not powers of three (Sec. 4.4): the number of blocks every rank forwards per
     step and direction, counted by the tree emulations of nonpow3 (the ring's mailbox form, the
     torus's gather form with one column per block), each m / (n D) again;
+  * latency-optimal variant on sides that are not powers of three: every message carries the
+    partials its receiver takes from the sender (latency_nonpow3), each m / D;
   * the Bruck comparison pattern on a ring (Sec. 2.4, Table 1): whole segments to the offsets
     +3^k and +2 3^k, or Algorithm 1's blocks for its bandwidth-optimal form (Sec. 2.4 says its
     data follows Trivance's pattern), for the threefold-congestion pin only.
@@ -85,6 +87,29 @@ def _messages_pow3(dims, variant):
     return len(plist), out
 
 
+def _messages_latency_tree(dims):
+    """Latency-optimal schedule on sides that are not all powers of three: every message carries
+    the distinct partials its receiver takes from the sender (latency_nonpow3), each m / D."""
+    from . import latency_nonpow3
+
+    dims = tuple(int(x) for x in dims)
+    D = len(dims)
+    n = int(np.prod(dims))
+    out = []
+    S = 0
+    for c in range(D):
+        rot = nonpow3.torus_rotation(dims, c)
+        S = len(rot)
+        for t, ((dim, k), (plus, minus)) in enumerate(zip(rot, latency_nonpow3.message_slots(dims, c))):
+            dist = nonpow3.distances(dims[dim])[k]
+            for r in range(n):
+                if plus:
+                    out.append((t, r, dim, +dist, Fraction(plus, D)))
+                if minus:
+                    out.append((t, r, dim, -dist, Fraction(minus, D)))
+    return S, out
+
+
 def _messages_tree(dims):
     """The same list for the Sec. 4.4 trees, from the emulations' per-message block counts."""
     dims = tuple(int(x) for x in dims)
@@ -132,6 +157,8 @@ def link_bytes(dims, variant: str, routing: str = "scheduled") -> np.ndarray:
     D = len(dims)
     if variant == "B" and nonpow3.is_tree(dims):
         P, msgs = _messages_tree(dims)
+    elif variant == "L" and nonpow3.is_tree(dims):
+        P, msgs = _messages_latency_tree(dims)
     else:
         P, msgs = _messages_pow3(dims, variant)
     acc = np.empty((P, n, 2 * D), dtype=object)

@@ -80,6 +80,12 @@ def _lib():
         "trivance_allreduce_emulated": (ctypes.c_int, [P, ctypes.c_int, i64, ctypes.c_int, P, P]),
         "trivance_allreduce_emulated_steps": (ctypes.c_int, [P, ctypes.c_int, i64, ctypes.c_int,
                                                              P, P, ctypes.c_int, ctypes.c_int]),
+        "trivance_workspace_bytes": (i64, [P, i64, ctypes.c_int]),
+        "trivance_allreduce_emulated_ws": (ctypes.c_int, [P, ctypes.c_int, i64, ctypes.c_int, P, P,
+                                                          i64, P]),
+        "trivance_allreduce_emulated_steps_ws": (ctypes.c_int, [P, ctypes.c_int, i64, ctypes.c_int,
+                                                                P, P, i64, P, ctypes.c_int,
+                                                                ctypes.c_int]),
         "trivance_congestion": (i64, [P, ctypes.POINTER(Topology), ctypes.POINTER(i64), i64]),
         "trivance_congestion_device": (ctypes.c_int, [P, ctypes.POINTER(Topology), P, i64, P]),
         "trivance_congestion_noalloc": (i64, [P, ctypes.POINTER(Topology), ctypes.POINTER(i64), i64]),
@@ -105,7 +111,9 @@ def exported_symbols() -> list:
              "trivance_plan_num_passes", "trivance_plan_step", "trivance_plan_step_index",
              "trivance_plan_with_dispatch_limit", "trivance_block_range",
              "trivance_algorithmic_bytes", "trivance_pass_bytes", "trivance_allreduce_emulated",
-             "trivance_allreduce_emulated_steps", "trivance_congestion",
+             "trivance_allreduce_emulated_steps", "trivance_workspace_bytes",
+             "trivance_allreduce_emulated_ws", "trivance_allreduce_emulated_steps_ws",
+             "trivance_congestion",
              "trivance_congestion_device", "trivance_congestion_noalloc", "trivance_fill_hash_uniform",
              "trivance_copy_device", "trivance_cost_model", "trivance_strerror"]
     return [n for n in names if hasattr(lib, n)]
@@ -235,6 +243,41 @@ def trivance_allreduce_emulated_steps(buffers, plan: Plan, pass_begin: int, pass
     _check(_lib().trivance_allreduce_emulated_steps(ptr, n, E, dt, plan.handle,
                                                     _stream_ptr(stream), pass_begin, pass_end),
            "trivance_allreduce_emulated_steps")
+
+
+def trivance_workspace_bytes(plan: Plan, elems: int, dtype: int = F32) -> int:
+    return _check(_lib().trivance_workspace_bytes(plan.handle, elems, dtype),
+                  "trivance_workspace_bytes")
+
+
+def _workspace_args(workspace):
+    import torch
+
+    if workspace is None:
+        return ctypes.c_void_p(0), 0
+    if not isinstance(workspace, torch.Tensor) or not workspace.is_cuda or \
+            not workspace.is_contiguous():
+        raise TypeError("workspace must be a contiguous CUDA tensor")
+    return ctypes.c_void_p(workspace.data_ptr()), workspace.numel() * workspace.element_size()
+
+
+def trivance_allreduce_emulated_ws(buffers, plan: Plan, workspace, stream=None) -> None:
+    """In-place emulated AllReduce with a caller-owned device workspace (any contiguous CUDA tensor
+    of at least trivance_workspace_bytes bytes)."""
+    ptr, n, E, dt = _buffer_args(buffers, plan)
+    wp, wb = _workspace_args(workspace)
+    _check(_lib().trivance_allreduce_emulated_ws(ptr, n, E, dt, plan.handle, wp, wb,
+                                                 _stream_ptr(stream)),
+           "trivance_allreduce_emulated_ws")
+
+
+def trivance_allreduce_emulated_steps_ws(buffers, plan: Plan, workspace, pass_begin: int,
+                                         pass_end: int, stream=None) -> None:
+    ptr, n, E, dt = _buffer_args(buffers, plan)
+    wp, wb = _workspace_args(workspace)
+    _check(_lib().trivance_allreduce_emulated_steps_ws(ptr, n, E, dt, plan.handle, wp, wb,
+                                                       _stream_ptr(stream), pass_begin, pass_end),
+           "trivance_allreduce_emulated_steps_ws")
 
 
 def _topology(plan: Plan, routing: str) -> Topology:

@@ -231,6 +231,17 @@ int trivance_congestion_device(const trivance_plan_t* plan, const trivance_topol
         }
         for (int c = 0; c < trivance::kMaxDims; ++c) {
             a.dirs[p][c] = 3;
+            if (!plan->slots.empty() && c < plan->D) {
+                // latency-optimal slot programs: a rank sends towards + when some slot takes a
+                // part from the peer at -distance, towards - when some slot takes one from +
+                const trivance::SlotPass& sp = plan->slots[p];
+                int m = 0;
+                for (int i = 0; i < sp.nout[c]; ++i) {
+                    if (sp.left[c][i] >= 0) m |= 1;
+                    if (sp.right[c][i] >= 0) m |= 2;
+                }
+                a.dirs[p][c] = (uint8_t)m;
+            }
             if (plan->tree && c < plan->D) {
                 // a reduce-scatter step sends child -> parent (every rank sends towards a side
                 // when any offset of the active dimension's tree does); its all-gather step

@@ -11,7 +11,8 @@
 // and both directions.
 //
 // Message sizes (m bytes per rank, D collectives on m / D each, blocks of m / (n D)):
-//   latency-optimal   the whole segment, m / D (Sec. 4.2);
+//   latency-optimal   the whole segment, m / D (Sec. 4.2); on sides that are not powers of three,
+//                     one segment per distinct partial the receiver takes from the sender;
 //   bandwidth-optimal n / 3^(t+1) blocks at reduce-scatter and all-gather step t (Sec. 4.1 and the
 //                     closed form of Sec. 4.3; Lemma 1);
 //   tree steps        per direction, the offsets of the active dimension's tree that forward
@@ -32,7 +33,19 @@ double pass_peak(const trivance_plan_t* p, const trivance::Pass& ps) {
         const int a = ps.dim[c];
         const double hops = ps.distance[c];
         double plus = 0.0, minus = 0.0;  // bytes of one rank's message towards + and -
-        if (ps.phase == TRIVANCE_PHASE_LATENCY) {
+        if (ps.phase == TRIVANCE_PHASE_LATENCY && !p->slots.empty()) {
+            // slot programs: a message carries every distinct slot its receiver takes from it
+            const trivance::SlotPass& sp = p->slots[&ps - p->passes.data()];
+            bool to_plus[trivance::kMaxSlots] = {}, to_minus[trivance::kMaxSlots] = {};
+            for (int i = 0; i < sp.nout[c]; ++i) {
+                if (sp.left[c][i] >= 0) to_plus[sp.left[c][i]] = true;
+                if (sp.right[c][i] >= 0) to_minus[sp.right[c][i]] = true;
+            }
+            for (int i = 0; i < sp.nin[c]; ++i) {
+                plus += to_plus[i] ? seg : 0.0;
+                minus += to_minus[i] ? seg : 0.0;
+            }
+        } else if (ps.phase == TRIVANCE_PHASE_LATENCY) {
             plus = minus = seg;
         } else if (!p->tree) {
             plus = minus = seg * (double)ps.kept_per_rank / p->n;

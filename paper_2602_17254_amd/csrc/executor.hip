@@ -710,6 +710,72 @@ __global__ __launch_bounds__(64) void tree_step_kernel(T* __restrict__ buf, Tree
 }
 
 // ---------------------------------------------------------------------------------------------
+// Latency-optimal step on sides that are not powers of three (Sec. 4.2 with Sec. 4.4): every rank
+// keeps a few partial sums ("slots", see plan.cpp) per collective. Output slot i of rank x is the
+// joint reduction (own + left) + right of input slot own[i] of x, left[i] of the peer at -distance
+// and right[i] of the peer at +distance along the collective's active dimension (absent terms
+// skipped). Inputs and outputs are different state arrays (slot s of a state is an [n][elems]
+// array at s * n * elems), so the pass has no in-place hazard. One wave handles 64 column vectors
+// of one rank of one collective and computes all its output slots.
+struct SlotArgs {
+    int64_t elems;
+    int64_t seg_g[kMaxDims + 1];
+    int64_t slot_stride;  // elements from one slot array to the next: n * elems
+    int n;
+    int D;
+    uint32_t colblocks;   // column blocks of 64 vectors per rank (largest segment)
+    uint32_t units;       // D * n * colblocks
+    int act[kMaxDims], dist[kMaxDims], side[kMaxDims], stride[kMaxDims], nout[kMaxDims];
+    int8_t own[kMaxDims][kMaxSlots], left[kMaxDims][kMaxSlots], right[kMaxDims][kMaxSlots];
+    uint32_t wg_base;
+};
+static_assert(sizeof(SlotArgs) <= 4096, "slot-step kernel arguments above 4 KiB");
+
+template <typename T, int VEC>
+__global__ __launch_bounds__(64) void slot_step_kernel(T* __restrict__ out,
+                                                      const T* __restrict__ in, SlotArgs a) {
+    using V = Vec<T, VEC>;
+    const uint32_t unit = a.wg_base + blockIdx.x;
+    if (unit >= a.units) return;
+    const uint32_t cb = unit % a.colblocks;
+    const uint32_t rest = unit / a.colblocks;
+    const int x = (int)(rest % (uint32_t)a.n);
+    const int c = (int)(rest / (uint32_t)a.n);
+    const int64_t E = a.elems;
+    const int64_t seg_b = imin64(a.seg_g[c] * kGranule, E);
+    const int64_t seg_e = imin64(a.seg_g[c + 1] * kGranule, E);
+    const int64_t col = seg_b + ((int64_t)cb * 64 + threadIdx.x) * VEC;
+    if (col >= seg_e) return;
+    const int stride = a.stride[a.act[c]], side = a.side[a.act[c]], dist = a.dist[c];
+    const int xa = (x / stride) % side;
+    const int xl = x + ((xa >= dist ? -dist : side - dist) * stride);
+    const int xr = x + ((xa + dist < side ? dist : dist - side) * stride);
+    const T* const own_row = in + (int64_t)x * E + col;
+    const T* const left_row = in + (int64_t)xl * E + col;
+    const T* const right_row = in + (int64_t)xr * E + col;
+    T* const out_row = out + (int64_t)x * E + col;
+    for (int i = 0; i < a.nout[c]; ++i) {
+        const int so = a.own[c][i], sl = a.left[c][i], sr = a.right[c][i];
+        V acc;
+        bool have = false;
+        if (so >= 0) {
+            acc = ld<T, VEC>(own_row + so * a.slot_stride);
+            have = true;
+        }
+        if (sl >= 0) {
+            const V v = ld<T, VEC>(left_row + sl * a.slot_stride);
+            acc = have ? vadd(acc, v) : v;
+            have = true;
+        }
+        if (sr >= 0) {
+            const V v = ld<T, VEC>(right_row + sr * a.slot_stride);
+            acc = have ? vadd(acc, v) : v;
+        }
+        st<T, VEC, true>(out_row + (int64_t)i * a.slot_stride, acc);
+    }
+}
+
+// ---------------------------------------------------------------------------------------------
 // Host side.
 
 // Where and how a call's launches go: the stream, and the most work-items of one dispatch (the
@@ -1066,9 +1132,76 @@ int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t
     }
 }
 
+// Workspace halves of a slot plan: state t (0 < t < S) lives in half (t - 1) % 2; a one-pass plan
+// writes its result to half 0 and copies it back (input and output must not alias).
+inline int slot_halves(const trivance_plan_t* p) { return p->S >= 3 ? 2 : (p->S >= 1 ? 1 : 0); }
+
+template <typename T, int VEC>
+int run_slot_passes(T* buf, int64_t elems, const trivance_plan_t* p, T* ws, hipStream_t stream,
+                    int pb, int pe) {
+    const Exec x{stream, p->dispatch_items};
+    SlotArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.elems = elems;
+    a.n = p->n;
+    a.D = p->D;
+    a.slot_stride = (int64_t)p->n * elems;
+    const int64_t G = (elems + kGranule - 1) / kGranule;
+    int64_t max_seg = 0;
+    for (int c = 0; c <= p->D; ++c) a.seg_g[c] = (int64_t)c * G / p->D;
+    for (int c = 0; c < p->D; ++c)
+        max_seg = std::max(max_seg, std::min(a.seg_g[c + 1] * kGranule, elems) -
+                                        std::min(a.seg_g[c] * kGranule, elems));
+    const int64_t vecs = (max_seg + VEC - 1) / VEC;
+    a.colblocks = (uint32_t)std::max<int64_t>(1, (vecs + 63) / 64);
+    const int64_t units = (int64_t)p->D * p->n * a.colblocks;
+    if (units >= ((int64_t)1 << 31)) return TRIVANCE_EUNSUPPORTED;
+    a.units = (uint32_t)units;
+    const int64_t half = (int64_t)p->max_slots * a.slot_stride;
+    const int S = p->S;
+    for (int pi = pb; pi < pe; ++pi) {
+        const Pass& ps = p->passes[pi];
+        const SlotPass& sp = p->slots[pi];
+        for (int c = 0; c < p->D; ++c) {
+            a.act[c] = ps.dim[c];
+            a.dist[c] = ps.distance[c];
+            a.nout[c] = sp.nout[c];
+            for (int i = 0; i < kMaxSlots; ++i) {
+                a.own[c][i] = sp.own[c][i];
+                a.left[c][i] = sp.left[c][i];
+                a.right[c][i] = sp.right[c][i];
+            }
+        }
+        for (int d = 0; d < kMaxDims; ++d) {
+            a.side[d] = d < p->D ? p->dims[d] : 1;
+            a.stride[d] = d < p->D ? p->strides[d] : 1;
+        }
+        const T* in = pi == 0 ? buf : ws + ((pi - 1) % 2) * half;
+        T* out = (pi == S - 1 && S > 1) ? buf : ws + (pi % 2) * half;
+        hipError_t err = hipSuccess;
+        for_each_dispatch(a.units, 64, x.items, [&](uint32_t first, uint32_t count) {
+            a.wg_base = first;
+            hipLaunchKernelGGL((slot_step_kernel<T, VEC>), dim3(count), dim3(64), 0, x.stream, out,
+                               in, a);
+            err = hipGetLastError();
+            return err == hipSuccess;
+        });
+        if (err != hipSuccess) return TRIVANCE_EHIP;
+        if (S == 1 && hipMemcpyAsync(buf, ws, (size_t)a.slot_stride * sizeof(T),
+                                     hipMemcpyDeviceToDevice, stream) != hipSuccess)
+            return TRIVANCE_EHIP;
+    }
+    return TRIVANCE_OK;
+}
+
 template <typename T>
-int run_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stream, int pb,
+int run_passes(T* buf, int64_t elems, const trivance_plan_t* p, T* ws, hipStream_t stream, int pb,
                int pe) {
+    if (!p->slots.empty()) {
+        if (elems % 4 == 0 && (uintptr_t)buf % 16 == 0 && (uintptr_t)ws % 16 == 0)
+            return run_slot_passes<T, 4>(buf, elems, p, ws, stream, pb, pe);
+        return run_slot_passes<T, 1>(buf, elems, p, ws, stream, pb, pe);
+    }
     if (p->tree) {
         if (elems % 4 == 0 && (uintptr_t)buf % 16 == 0)
             return run_tree_passes<T, 4>(buf, elems, p, stream, pb, pe);
@@ -1085,9 +1218,17 @@ int run_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t stre
 
 extern "C" {
 
-int trivance_allreduce_emulated_steps(void* buffers, int n, int64_t elems, int dtype,
-                                      const trivance_plan_t* plan, void* stream, int pass_begin,
-                                      int pass_end) {
+int64_t trivance_workspace_bytes(const trivance_plan_t* plan, int64_t elems, int dtype) {
+    if (!plan || elems < 0) return TRIVANCE_EINVAL;
+    if (dtype != TRIVANCE_F32 && dtype != TRIVANCE_I32) return TRIVANCE_EINVAL;
+    if (plan->slots.empty()) return 0;
+    return (int64_t)trivance::slot_halves(plan) * plan->max_slots * plan->n * elems * 4;
+}
+
+int trivance_allreduce_emulated_steps_ws(void* buffers, int n, int64_t elems, int dtype,
+                                         const trivance_plan_t* plan, void* workspace,
+                                         int64_t workspace_bytes, void* stream, int pass_begin,
+                                         int pass_end) {
     if (!plan || n != plan->n || elems < 0) return TRIVANCE_EINVAL;
     if (dtype != TRIVANCE_F32 && dtype != TRIVANCE_I32) return TRIVANCE_EINVAL;
     const int np = (int)plan->passes.size();
@@ -1095,12 +1236,30 @@ int trivance_allreduce_emulated_steps(void* buffers, int n, int64_t elems, int d
     if (plan->variant == TRIVANCE_BRUCK_REF) return TRIVANCE_EUNSUPPORTED;
     if (elems == 0 || pass_begin == pass_end) return TRIVANCE_OK;
     if (!buffers) return TRIVANCE_EINVAL;
+    const int64_t need = trivance_workspace_bytes(plan, elems, dtype);
+    if (workspace_bytes < need || (need > 0 && !workspace)) return TRIVANCE_ESIZE;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (dtype == TRIVANCE_F32)
-        return trivance::run_passes<float>(static_cast<float*>(buffers), elems, plan, s,
-                                           pass_begin, pass_end);
-    return trivance::run_passes<int>(static_cast<int*>(buffers), elems, plan, s, pass_begin,
-                                     pass_end);
+        return trivance::run_passes<float>(static_cast<float*>(buffers), elems, plan,
+                                           static_cast<float*>(workspace), s, pass_begin, pass_end);
+    return trivance::run_passes<int>(static_cast<int*>(buffers), elems, plan,
+                                     static_cast<int*>(workspace), s, pass_begin, pass_end);
+}
+
+int trivance_allreduce_emulated_ws(void* buffers, int n, int64_t elems, int dtype,
+                                   const trivance_plan_t* plan, void* workspace,
+                                   int64_t workspace_bytes, void* stream) {
+    if (!plan) return TRIVANCE_EINVAL;
+    return trivance_allreduce_emulated_steps_ws(buffers, n, elems, dtype, plan, workspace,
+                                                workspace_bytes, stream, 0,
+                                                (int)plan->passes.size());
+}
+
+int trivance_allreduce_emulated_steps(void* buffers, int n, int64_t elems, int dtype,
+                                      const trivance_plan_t* plan, void* stream, int pass_begin,
+                                      int pass_end) {
+    return trivance_allreduce_emulated_steps_ws(buffers, n, elems, dtype, plan, nullptr, 0, stream,
+                                                pass_begin, pass_end);
 }
 
 int trivance_allreduce_emulated(void* buffers, int n, int64_t elems, int dtype,

@@ -274,6 +274,172 @@ int build_tree_plan(trivance_plan_t* p) {
     return TRIVANCE_OK;
 }
 
+// ---- latency-optimal variant on sides that are not powers of three (Sec. 4.2 with Sec. 4.4) ----
+//
+// A rank keeps partial sums ("slots") over boxes of offsets relative to itself (one interval per
+// dimension). The result is the whole torus; going backwards through the passes, a box needed after
+// a full step at distance 3^k along dimension a is the joint reduction of its parts inside the left
+// peer's previous window, the own previous window and the right peer's (three disjoint windows that
+// tile the new one, Appendix A); after the final step along a (distance d), the whole ring along a
+// is the own window [-R, R] plus the offsets above R from the peer at +d (the top of that peer's
+// window) and those below -R from the peer at -d, offsets taken in (-side/2, side/2]. Every part is
+// again a box the sender holds before the pass; the boxes needed before pass t are the slots of
+// state t. On powers of three the window is the only slot (the ordinary schedule).
+
+struct Ivl {
+    int lo, hi;  // offsets lo..hi; empty when lo > hi
+    bool empty() const { return lo > hi; }
+    bool operator==(const Ivl& o) const { return lo == o.lo && hi == o.hi; }
+};
+
+Ivl meet(Ivl a, Ivl b) { return Ivl{std::max(a.lo, b.lo), std::min(a.hi, b.hi)}; }
+
+struct SlotBox {
+    Ivl iv[kMaxDims];
+    bool operator==(const SlotBox& o) const {
+        for (int d = 0; d < kMaxDims; ++d)
+            if (!(iv[d] == o.iv[d])) return false;
+        return true;
+    }
+};
+
+struct SideSteps {
+    int side = 1, f = 0, d = 0;  // full steps, final distance (0: none)
+    int steps() const { return side == 1 ? 0 : f + (d ? 1 : 0); }
+    int dist(int k) const { return k < f ? ipow3(k) : d; }
+    // offsets covered after `taken` steps along this side (Lemma 2 windows, then the whole ring)
+    Ivl window(int taken) const {
+        if (side == 1) return Ivl{0, 0};
+        if (taken > f) {
+            const int lo = -((side - 1) / 2);
+            return Ivl{lo, lo + side - 1};
+        }
+        const int R = (ipow3(taken) - 1) / 2;
+        return Ivl{-R, R};
+    }
+};
+
+SideSteps side_steps(int side) {
+    SideSteps ss;
+    ss.side = side;
+    if (side == 1) return ss;
+    int pw = 1;
+    while (pw * 3 <= side) {
+        pw *= 3;
+        ss.f += 1;
+    }
+    ss.d = pw == side ? 0 : (side - pw + 1) / 2;
+    return ss;
+}
+
+int build_latency_slot_plan(trivance_plan_t* p) {
+    const int D = p->D;
+    SideSteps ss[kMaxDims];
+    p->S = 0;
+    for (int d = 0; d < D; ++d) {
+        ss[d] = side_steps(p->dims[d]);
+        p->S += ss[d].steps();
+    }
+    const int S = p->S;
+    if (S > 40) return TRIVANCE_EUNSUPPORTED;
+    std::vector<Pass> passes(S);
+    std::vector<trivance::SlotPass> sp(S);
+    for (int t = 0; t < S; ++t) {
+        passes[t] = Pass{};
+        passes[t].phase = TRIVANCE_PHASE_LATENCY;
+        passes[t].step = t;
+        for (int c = 0; c < kMaxDims; ++c) {
+            passes[t].distance[c] = 1;
+            for (int dd = 0; dd < kMaxDims; ++dd) passes[t].modulus[c][dd] = 1;
+        }
+        sp[t] = trivance::SlotPass{};
+    }
+    p->max_slots = 1;
+    for (int c = 0; c < D; ++c) {
+        // rotation: the first dimension, cyclically from (c + t) mod D, with steps left
+        std::vector<std::vector<int>> taken(S + 1, std::vector<int>(D, 0));
+        std::vector<int> act(S), kk(S);
+        for (int t = 0; t < S; ++t) {
+            int dsel = -1;
+            for (int i = 0; i < D && dsel < 0; ++i) {
+                const int cand = (c + t + i) % D;
+                if (taken[t][cand] < ss[cand].steps()) dsel = cand;
+            }
+            act[t] = dsel;
+            kk[t] = taken[t][dsel];
+            taken[t + 1] = taken[t];
+            taken[t + 1][dsel] += 1;
+            Pass& ps = passes[t];
+            ps.dim[c] = dsel;
+            ps.dim_step[c] = kk[t];
+            ps.distance[c] = ss[dsel].dist(kk[t]);
+            for (int dd = 0; dd < D; ++dd) ps.taken[c][dd] = taken[t][dd];
+        }
+        auto window_box = [&](int t) {
+            SlotBox b{};
+            for (int dd = 0; dd < kMaxDims; ++dd)
+                b.iv[dd] = dd < D ? ss[dd].window(taken[t][dd]) : Ivl{0, 0};
+            return b;
+        };
+        std::vector<SlotBox> need{window_box(S)};
+        for (int t = S - 1; t >= 0; --t) {
+            const int a = act[t];
+            const int dist = ss[a].dist(kk[t]);
+            const Ivl prev = ss[a].window(taken[t][a]);
+            const Ivl cur = ss[a].window(taken[t + 1][a]);
+            const bool final_step = ss[a].d != 0 && kk[t] == ss[a].f;
+            std::vector<SlotBox> parts{window_box(t)};
+            auto index_of = [&](const SlotBox& b) {
+                for (size_t i = 0; i < parts.size(); ++i)
+                    if (parts[i] == b) return (int)i;
+                parts.push_back(b);
+                return (int)parts.size() - 1;
+            };
+            if ((int)need.size() > trivance::kMaxSlots) return TRIVANCE_EUNSUPPORTED;
+            sp[t].nout[c] = (int)need.size();
+            for (size_t i = 0; i < need.size(); ++i) {
+                const Ivl I = need[i].iv[a];
+                if (I.lo < cur.lo || I.hi > cur.hi) return TRIVANCE_EUNSUPPORTED;  // not a window part
+                Ivl own, left, right;
+                if (final_step) {
+                    if (!(I == cur)) return TRIVANCE_EUNSUPPORTED;
+                    own = prev;
+                    left = Ivl{cur.lo, prev.lo - 1};   // beyond -R: from the peer at -d
+                    right = Ivl{prev.hi + 1, cur.hi};  // beyond +R: from the peer at +d
+                } else {
+                    own = meet(I, prev);
+                    left = meet(I, Ivl{cur.lo, prev.lo - 1});
+                    right = meet(I, Ivl{prev.hi + 1, cur.hi});
+                }
+                const Ivl pieces[3] = {own, left, right};
+                const int shift[3] = {0, +dist, -dist};  // into the sender's own frame
+                int idx[3];
+                for (int q = 0; q < 3; ++q) {
+                    idx[q] = -1;
+                    if (pieces[q].empty()) continue;
+                    SlotBox b = need[i];
+                    b.iv[a] = Ivl{pieces[q].lo + shift[q], pieces[q].hi + shift[q]};
+                    if (b.iv[a].lo < prev.lo || b.iv[a].hi > prev.hi) return TRIVANCE_EUNSUPPORTED;
+                    idx[q] = index_of(b);
+                }
+                sp[t].own[c][i] = (int8_t)idx[0];
+                sp[t].left[c][i] = (int8_t)idx[1];
+                sp[t].right[c][i] = (int8_t)idx[2];
+            }
+            if ((int)parts.size() > trivance::kMaxSlots) return TRIVANCE_EUNSUPPORTED;
+            sp[t].nin[c] = (int)parts.size();
+            p->max_slots = std::max(p->max_slots, (int)parts.size());
+            need.swap(parts);
+        }
+        // before the first pass a rank holds only its own value
+        SlotBox start{};
+        if (need.size() != 1 || !(need[0] == start)) return TRIVANCE_EUNSUPPORTED;
+    }
+    p->passes = passes;
+    p->slots = sp;
+    return TRIVANCE_OK;
+}
+
 }  // namespace
 
 namespace trivance {
@@ -358,10 +524,10 @@ int trivance_plan_ex(int n, const int* torus_dims, int ndims, int variant, unsig
     for (int d = 0; d < D; ++d) pow3 = pow3 && log3_exact(dims[d]) >= 0;
     if ((flags & TRIVANCE_PLACE_BY_SCHEDULE) && (!pow3 || variant != TRIVANCE_BANDWIDTH_OPT))
         return TRIVANCE_EUNSUPPORTED;
-    // Sec. 4.4 (sides that are not powers of three): bandwidth-optimal variant only
+    // Sec. 4.4 (sides that are not powers of three): reduction trees (bandwidth-optimal) or slot
+    // programs (latency-optimal)
     if (!pow3) {
-        if (variant != TRIVANCE_BANDWIDTH_OPT || D > trivance::kMaxTreeDims)
-            return TRIVANCE_EUNSUPPORTED;
+        if (variant == TRIVANCE_BRUCK_REF || D > trivance::kMaxTreeDims) return TRIVANCE_EUNSUPPORTED;
         for (int d = 0; d < D; ++d)
             if (dims[d] > trivance::kMaxTreeSide) return TRIVANCE_EUNSUPPORTED;
     }
@@ -381,7 +547,7 @@ int trivance_plan_ex(int n, const int* torus_dims, int ndims, int variant, unsig
         }
         int rc;
         try {
-            rc = build_tree_plan(p);
+            rc = variant == TRIVANCE_BANDWIDTH_OPT ? build_tree_plan(p) : build_latency_slot_plan(p);
         } catch (const std::bad_alloc&) {
             rc = TRIVANCE_ENOMEM;
         }
@@ -491,6 +657,18 @@ int64_t trivance_pass_bytes(const trivance_plan_t* plan, int64_t elems, int dtyp
     const int64_t w = 4;
     const Pass& ps = plan->passes[pass];
     const int64_t n = plan->n;
+    if (ps.phase == TRIVANCE_PHASE_LATENCY && !plan->slots.empty()) {
+        // every rank reads each slot it holds before the pass once and writes each slot it holds
+        // after it once, over its collective's segment
+        const trivance::SlotPass& sp = plan->slots[pass];
+        int64_t acc = 0;
+        for (int c = 0; c < plan->D; ++c) {
+            int64_t b, e;
+            trivance::block_bounds(plan, elems, c, -1, &b, &e);
+            acc += (int64_t)(sp.nin[c] + sp.nout[c]) * n * (e - b);
+        }
+        return acc * w;
+    }
     if (ps.phase == TRIVANCE_PHASE_LATENCY) return 2 * n * elems * w;
     if (plan->tree) {
         // Collective c's pass touches, for every block j of its segment, the ranks j + o with o

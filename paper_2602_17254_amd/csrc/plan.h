@@ -29,6 +29,17 @@ struct Pass {
     int taken[kMaxDims][kMaxDims];
 };
 
+// Latency-optimal plans with a side that is not a power of three: every rank keeps several partial
+// sums ("slots") per collective between passes. Output slot i of a pass is the joint reduction
+// (own + left) + right of the input slots own[i] of the rank itself, left[i] of its peer at
+// -distance and right[i] of its peer at +distance (-1: that term is absent).
+constexpr int kMaxSlots = 64;
+struct SlotPass {
+    int nin[kMaxDims];   // slots per rank before the pass, per collective
+    int nout[kMaxDims];  // after it
+    int8_t own[kMaxDims][kMaxSlots], left[kMaxDims][kMaxSlots], right[kMaxDims][kMaxSlots];
+};
+
 }  // namespace trivance
 
 namespace trivance {
@@ -71,6 +82,10 @@ struct trivance_plan {
     bool placed = false;
     // Most work-items one kernel dispatch may hold (trivance_plan_with_dispatch_limit).
     int64_t dispatch_items = (int64_t)1 << 31;
+    // Latency-optimal plans with a side that is not a power of three: the slot program of every
+    // pass (same length as `passes`), and the most slots any state between passes holds.
+    std::vector<trivance::SlotPass> slots;
+    int max_slots = 0;
 };
 
 namespace trivance {

@@ -70,7 +70,13 @@ int main(void) {
 
     /* errors */
     trivance_plan_t* r = NULL;
-    CHECK(trivance_plan(8, NULL, 0, TRIVANCE_LATENCY_OPT, &r) == TRIVANCE_EUNSUPPORTED && r == NULL);
+    CHECK(trivance_plan(8, NULL, 0, TRIVANCE_BRUCK_REF, &r) == TRIVANCE_EUNSUPPORTED && r == NULL);
+    /* the latency-optimal variant on a ring of 8 keeps partials in a workspace (Sec. 4.4) */
+    CHECK(trivance_plan(8, NULL, 0, TRIVANCE_LATENCY_OPT, &r) == TRIVANCE_OK && r != NULL);
+    CHECK(trivance_plan_num_passes(r) == 2);
+    CHECK(trivance_workspace_bytes(r, 100, TRIVANCE_F32) == 2 * 8 * 100 * 4);
+    trivance_plan_destroy(r);
+    r = NULL;
     CHECK(trivance_plan(80, dims, 2, TRIVANCE_LATENCY_OPT, &r) == TRIVANCE_EINVAL);
     CHECK(trivance_allreduce_emulated(NULL, 9, 0, TRIVANCE_F32, NULL, NULL) == TRIVANCE_EINVAL);
     CHECK(strcmp(trivance_strerror(TRIVANCE_ESIZE), "output buffer too small") == 0);

@@ -21,7 +21,14 @@ def run_hip(V: np.ndarray, dims, variant: str, placement: str = "natural",
     if dispatch_items is not None:
         plan = T.trivance_plan_with_dispatch_limit(plan, dispatch_items)
     buf = torch.from_numpy(np.ascontiguousarray(V)).cuda()
-    T.trivance_allreduce_emulated(buf, plan)
+    ws_bytes = T.trivance_workspace_bytes(plan, V.shape[1])
+    if ws_bytes:
+        # the partial sums of the latency-optimal variant on sides that are not powers of three;
+        # filled with NaN so that a read of stale contents would show
+        ws = torch.full(((ws_bytes + 3) // 4,), float("nan"), dtype=torch.float32, device="cuda")
+        T.trivance_allreduce_emulated_ws(buf, plan, ws)
+    else:
+        T.trivance_allreduce_emulated(buf, plan)
     torch.cuda.synchronize()
     return buf.cpu().numpy()
 
@@ -33,7 +40,11 @@ def assert_matches_oracle(got: np.ndarray, V: np.ndarray, dims, variant: str, co
     int32: bit-exact. fp32: |g - o| <= 1e-6 |o| elementwise (the oracle's order is the kernel's,
     so the difference is expected to be exactly zero, which is asserted as well), and every
     element within 4 S 2^-23 sum|v| of the fp64 sum."""
-    if variant == "L":
+    if variant == "L" and nonpow3.is_tree(dims):
+        from oracle import latency_nonpow3
+
+        want = latency_nonpow3.latency_optimal(V, dims, col_seg=col_seg)
+    elif variant == "L":
         want = allreduce.latency_optimal(V, dims, col_seg=col_seg)
     elif nonpow3.is_tree(dims) and len(dims) == 1 and dims[0] <= 300:
         want = nonpow3.bandwidth_optimal_ring(V, col_blk=col_blk)

@@ -85,10 +85,7 @@ def test_algorithmic_bytes(dims):
 
 def test_plan_errors():
     with pytest.raises(T.TrivanceError) as e:
-        T.trivance_plan((8,), "L")
-    assert e.value.status == -2
-    with pytest.raises(T.TrivanceError) as e:
-        T.trivance_plan((9, 8), "L")
+        T.trivance_plan((8,), "BRUCK")
     assert e.value.status == -2
     with pytest.raises(T.TrivanceError) as e:
         T.trivance_plan((9, 9), "BRUCK")
@@ -256,8 +253,9 @@ def test_nonpower3_torus_plan_matches_oracle(dims):
 
 
 def test_nonpower3_limits():
-    for dims, variant in [((8,), "L"), ((8,), "BRUCK"), ((8, 8), "L"), ((2201,), "B"),
-                          ((2, 2, 2, 2, 2), "B"), ((2201, 2), "B"), ((1000, 1000, 1000), "B")]:
+    for dims, variant in [((8,), "BRUCK"), ((2201,), "B"), ((2201,), "L"), ((5, 5, 5, 5), "L"),
+                          ((2, 2, 2, 2, 2), "B"), ((2, 2, 2, 2, 2), "L"), ((2201, 2), "B"),
+                          ((1000, 1000, 1000), "B")]:
         with pytest.raises(T.TrivanceError) as e:
             T.trivance_plan(dims, variant)
         assert e.value.status == -2
@@ -329,3 +327,67 @@ def test_copy_helper_rejects_bad_arguments_before_any_launch():
     assert lib.trivance_copy_device(None, P(8192), 16, None) == EINVAL
     assert lib.trivance_copy_device(P(4096), P(4096 + 32), 64, None) == EINVAL  # overlap
     assert lib.trivance_copy_device(P(4096 + 32), P(4096), 64, None) == EINVAL  # overlap
+
+
+# ---- latency-optimal plans on sides that are not powers of three (slot programs) ----
+
+LATENCY_TREES = [(2,), (4,), (5,), (7,), (8,), (10,), (20,), (32,), (64,), (100,), (728,),
+                 (4, 4), (2, 3), (3, 8), (8, 3), (5, 7), (1, 8), (2, 3, 4), (4, 4, 4), (2, 2, 2, 2),
+                 (32, 32), (8, 64), (16, 16, 16), (10, 3, 3)]
+
+
+@pytest.mark.parametrize("dims", LATENCY_TREES, ids=lambda d: "x".join(map(str, d)))
+def test_latency_slot_plan_matches_oracle_program(dims):
+    """The plan's passes (dimension and distance per collective, step index) equal the oracle's
+    rotation; per pass and collective, the byte accounting (every partial held before the pass
+    read once, every one after it written once) equals the oracle's partial counts; the
+    workspace holds the most partials of any state between passes."""
+    from oracle import latency_nonpow3, nonpow3, partition
+
+    dims = tuple(dims)
+    D = len(dims)
+    n = int(np.prod(dims))
+    p = T.trivance_plan(dims, "L")
+    S = sum(nonpow3.dim_steps(s) for s in dims)
+    assert p.num_steps == S and p.num_passes == S
+    E = 64 * D * 3 + 37  # unequal segments and a ragged tail
+    seg = [e - b for b, e in partition.segment_bounds(E, D)]
+    progs = [latency_nonpow3.program(dims, c) for c in range(D)]
+    rot = [nonpow3.torus_rotation(dims, c) for c in range(D)]
+    most = 1
+    for t in range(S):
+        assert T.trivance_plan_step_index(p, t) == t
+        want = 0
+        for c in range(D):
+            phase, dim, d = T.trivance_plan_step(p, t, c)
+            assert (phase, dim, d) == (0, rot[c][t][0], nonpow3.distances(dims[rot[c][t][0]])[rot[c][t][1]])
+            needed = progs[c][0]
+            want += (len(needed[t]) + len(needed[t + 1])) * n * seg[c] * 4
+            most = max(most, len(needed[t]))
+        assert T.trivance_pass_bytes(p, E, t) == want
+    halves = 2 if S >= 3 else 1
+    assert T.trivance_workspace_bytes(p, E) == halves * most * n * E * 4
+    assert T.trivance_workspace_bytes(p, E, T.I32) == halves * most * n * E * 4
+
+
+def test_latency_slot_plan_needs_its_workspace():
+    """The in-place entry points refuse a plan that keeps partials between passes (ESIZE), before
+    any launch; so does the workspace form with a workspace below the required size."""
+    import ctypes
+
+    lib = T.binding._lib()
+    p = T.trivance_plan((8,), "L")
+    need = T.trivance_workspace_bytes(p, 1000)
+    assert need > 0
+    fake = ctypes.c_void_p(1 << 40)  # never dereferenced: the size check comes first
+    assert lib.trivance_allreduce_emulated(fake, 8, 1000, 0, p.handle, None) == -5
+    assert lib.trivance_allreduce_emulated_steps(fake, 8, 1000, 0, p.handle, None, 0, 1) == -5
+    assert lib.trivance_allreduce_emulated_ws(fake, 8, 1000, 0, p.handle, fake, need - 1, None) == -5
+    assert lib.trivance_allreduce_emulated_ws(fake, 8, 1000, 0, p.handle, None, need, None) == -5
+    # elems == 0 is a no-op, and plans that run in place need no workspace
+    assert lib.trivance_allreduce_emulated(fake, 8, 0, 0, p.handle, None) == 0
+    for dims, v in [((9,), "L"), ((8,), "B"), ((27, 27), "B"), ((9, 3), "L")]:
+        assert T.trivance_workspace_bytes(T.trivance_plan(dims, v), 12345) == 0
+    assert lib.trivance_workspace_bytes(None, 10, 0) == -1
+    assert lib.trivance_workspace_bytes(p.handle, -1, 0) == -1
+    assert lib.trivance_workspace_bytes(p.handle, 10, 7) == -1

@@ -106,7 +106,10 @@ SHAPES = [((9,), "L"), ((81,), "L"), ((243,), "B"), ((27, 27), "B"), ((9, 9, 9),
           ((8,), "B"), ((32, 32), "B"), ((8, 64), "B"),
           ((7,), "B"), ((64,), "B"), ((100,), "B"), ((4, 8), "B"), ((5, 7), "B"), ((2, 3, 4), "B"),
           ((27, 27), "L"), ((9, 9, 9), "L"), ((3, 9), "L"), ((9, 27), "L"), ((3, 9), "B"),
-          ((3, 3, 9), "B"), ((1, 8), "B"), ((1,), "B"), ((3,), "L")]
+          ((3, 3, 9), "B"), ((1, 8), "B"), ((1,), "B"), ((3,), "L"),
+          # latency-optimal on sides that are not powers of three (messages with several partials)
+          ((2,), "L"), ((4,), "L"), ((7,), "L"), ((8,), "L"), ((32,), "L"), ((64,), "L"),
+          ((4, 4), "L"), ((5, 7), "L"), ((32, 32), "L"), ((8, 64), "L"), ((2, 3, 4), "L")]
 
 
 @pytest.mark.parametrize("dims,variant", SHAPES,

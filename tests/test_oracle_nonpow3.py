@@ -153,9 +153,14 @@ def test_congestion_uniform_and_final_equals_distance(n):
         assert (loads[S - 1] == d).all()
 
 
-def test_latency_variant_rejected():
+def test_latency_variant_dispatches_to_its_oracle():
+    from oracle import latency_nonpow3
+
+    V = np.random.default_rng(8).integers(-99, 99, size=(8, 77), dtype=np.int32)
+    np.testing.assert_array_equal(allreduce.allreduce(V, (8,), "L"),
+                                  latency_nonpow3.latency_optimal(V, (8,)))
     with pytest.raises(ValueError):
-        allreduce.allreduce(np.zeros((8, 4), np.float32), (8,), "L")
+        allreduce.allreduce(V, (8,), "X")
 
 
 # ---- tori with a side that is not a power of three ----
