@@ -110,7 +110,7 @@ def cpu_baseline(w, gpu_first_result_cols, cols, V_cols, seconds_target=10.0, ma
         seg, blk = partition.column_labels(w.elems, D, w.n, cols)
     def run():
         if w.variant == "L":
-            return allreduce.latency_optimal(V_cols, w.dims, col_seg=seg)
+            return allreduce.allreduce(V_cols, w.dims, "L", col_seg=seg)
         return allreduce.allreduce(V_cols, w.dims, "B", col_seg=seg, col_blk=blk)
 
     t0 = time.perf_counter()
@@ -231,12 +231,29 @@ def _all_finite(buf, rows=16):
     return all(bool(torch.isfinite(buf[r:r + rows]).all()) for r in range(0, buf.shape[0], rows))
 
 
-def _timed_steps(buf, plan, regen, groups, steps, stream):
-    """K AllReduces; before each, the inputs are restored (outside the events). Returns the
-    per-step, per-phase-group event times (ms) and the wall time of the whole region (s)."""
+def _workspace(plan, elems):
+    """The device workspace a plan needs (None when it runs in place)."""
     import torch
 
     import paper_2602_17254_amd as T
+
+    nbytes = T.trivance_workspace_bytes(plan, elems)
+    return torch.empty(nbytes, dtype=torch.uint8, device="cuda") if nbytes else None
+
+
+def _run_passes(buf, plan, ws, pb, pe, stream):
+    import paper_2602_17254_amd as T
+
+    if ws is None:
+        T.trivance_allreduce_emulated_steps(buf, plan, pb, pe, stream)
+    else:
+        T.trivance_allreduce_emulated_steps_ws(buf, plan, ws, pb, pe, stream)
+
+
+def _timed_steps(buf, plan, regen, groups, steps, stream, ws=None):
+    """K AllReduces; before each, the inputs are restored (outside the events). Returns the
+    per-step, per-phase-group event times (ms) and the wall time of the whole region (s)."""
+    import torch
 
     G = len(groups)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(G + 1)] for _ in range(steps)]
@@ -246,7 +263,7 @@ def _timed_steps(buf, plan, regen, groups, steps, stream):
         regen(stream)
         ev[k][0].record(stream)
         for g, (pb, pe, _) in enumerate(groups):
-            T.trivance_allreduce_emulated_steps(buf, plan, pb, pe, stream)
+            _run_passes(buf, plan, ws, pb, pe, stream)
             ev[k][g + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -272,11 +289,14 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
     # ---- inputs resident in HBM (untimed) ----
     _say(f"[bench] {w.name}: preparing inputs ({w.n} x {w.elems} {dtype})")
     buf, regen, V_host = _inputs_on_device(w, dtype)
+    ws = _workspace(plan, w.elems)
     stream = torch.cuda.current_stream()
 
     # ---- first run: result kept for the CPU-baseline comparison ----
     # about 15 s of single-core oracle work: fewer columns as the rank count grows
     budget = {"L": 2_097_152, "B": min(60_000, (1 << 24) // w.n)}[w.variant]
+    if w.variant == "L" and any(not _is_pow3(x) for x in w.dims):
+        budget = min(budget, (1 << 22) // w.n)  # the oracle keeps several partials per rank
     cols = _sample_for_baseline(w, min(budget, w.elems))
     if V_host is not None:
         V_cols = np.ascontiguousarray(V_host[:, cols])
@@ -284,7 +304,7 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
         V_cols = inputs.hash_uniform(w.seed, w.elems, np.arange(w.n), cols)
     del V_host
     regen(stream)
-    T.trivance_allreduce_emulated(buf, plan, stream)
+    _run_passes(buf, plan, ws, 0, P, stream)
     torch.cuda.synchronize()
     first_cols = None
     if with_cpu:
@@ -293,7 +313,7 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
     # ---- warmup (inputs restored before each AllReduce, like the timed steps) ----
     for _ in range(warmup):
         regen(stream)
-        T.trivance_allreduce_emulated(buf, plan, stream)
+        _run_passes(buf, plan, ws, 0, P, stream)
     torch.cuda.synchronize()
 
     # Passes of one phase run back to back with one kernel family (latency: every pass; reduce-
@@ -303,7 +323,7 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
 
     # ---- timed region: K AllReduces on freshly restored inputs, events on the launch stream ----
     _say(f"[bench] {w.name}: timing {steps} steps x {P} passes")
-    group_ms, wall = _timed_steps(buf, plan, regen, groups, steps, stream)
+    group_ms, wall = _timed_steps(buf, plan, regen, groups, steps, stream, ws)
     step_ms = group_ms.sum(axis=1)
     ms_per_step = float(step_ms.mean())
     value = alg_bytes / (ms_per_step * 1e-3) / 1e9
@@ -314,14 +334,14 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
     pev = [torch.cuda.Event(enable_timing=True) for _ in range(P + 1)]
     for p in range(P):
         pev[p].record(stream)
-        T.trivance_allreduce_emulated_steps(buf, plan, p, p + 1, stream)
+        _run_passes(buf, plan, ws, p, p + 1, stream)
     pev[P].record(stream)
     torch.cuda.synchronize()
     per_pass_ms = [pev[p].elapsed_time(pev[p + 1]) for p in range(P)]
 
     # dominant kernel: the family with the most time in the timed region
     tree = any(not _is_pow3(s) for s in w.dims)
-    names = {0: "latency_split_kernel",
+    names = {0: "slot_step_kernel" if tree else "latency_split_kernel",
              1: "tree_step_kernel<reduce>" if tree else "block_step_kernel<reduce>",
              2: "tree_step_kernel<copy>" if tree else "block_step_kernel<copy>"}
     dg = int(np.argmax(group_ms.sum(axis=0)))
@@ -387,7 +407,9 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
         "roofline": roofline,
         "cpu_baseline": None,
     }
-    del buf, regen
+    if ws is not None:
+        line["config"]["workspace_bytes"] = ws.numel()
+    del buf, regen, ws
     torch.cuda.empty_cache()
     ceiling = copy_ceiling()
     line["copy_ceiling"] = ceiling
@@ -529,13 +551,15 @@ def sweep(steps: int, warmup: int) -> None:
                 continue
             _say(f"[sweep] {'x'.join(map(str, dims))} {variant} {placement} {mib} MiB per rank")
             buf = torch.empty((n, E), dtype=torch.float32, device="cuda")
+            ws = _workspace(plan, E)
             T.trivance_fill_hash_uniform(buf, 7)
+            s0 = torch.cuda.current_stream()
             for _ in range(warmup):
-                T.trivance_allreduce_emulated(buf, plan)
+                _run_passes(buf, plan, ws, 0, plan.num_passes, s0)
             torch.cuda.synchronize()
             t0 = time.perf_counter()
             for _ in range(steps):
-                T.trivance_allreduce_emulated(buf, plan)
+                _run_passes(buf, plan, ws, 0, plan.num_passes, s0)
             torch.cuda.synchronize()
             ms = (time.perf_counter() - t0) * 1e3 / steps
             alg = T.trivance_algorithmic_bytes(plan, E)
@@ -545,7 +569,7 @@ def sweep(steps: int, warmup: int) -> None:
                               "ms_per_allreduce": round(ms, 4), "GBps": round(gbps, 1),
                               "pct_of_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
                               "resident_GB": round(n * E * 4 / 1e9, 2)}), flush=True)
-            del buf
+            del buf, ws
             torch.cuda.empty_cache()
 
 

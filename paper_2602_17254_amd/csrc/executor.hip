@@ -715,8 +715,14 @@ __global__ __launch_bounds__(64) void tree_step_kernel(T* __restrict__ buf, Tree
 // joint reduction (own + left) + right of input slot own[i] of x, left[i] of the peer at -distance
 // and right[i] of the peer at +distance along the collective's active dimension (absent terms
 // skipped). Inputs and outputs are different state arrays (slot s of a state is an [n][elems]
-// array at s * n * elems), so the pass has no in-place hazard. One wave handles 64 column vectors
-// of one rank of one collective and computes all its output slots.
+// array at s * n * elems), so the pass has no in-place hazard.
+//
+// One wave handles 64 column vectors of one rank of one collective and computes all its output
+// slots. Along the active dimension the ranks x, x + d, x + 2d, ... form cycles; units are
+// numbered so that consecutive ones are consecutive ranks of one cycle at the same columns, and
+// each XCD takes one contiguous range of units: the partials a wave reads from its peers at -d
+// and +d were just read by its neighbours in the schedule, so they come from the XCD's L2 rather
+// than HBM.
 struct SlotArgs {
     int64_t elems;
     int64_t seg_g[kMaxDims + 1];
@@ -726,6 +732,7 @@ struct SlotArgs {
     uint32_t colblocks;   // column blocks of 64 vectors per rank (largest segment)
     uint32_t units;       // D * n * colblocks
     int act[kMaxDims], dist[kMaxDims], side[kMaxDims], stride[kMaxDims], nout[kMaxDims];
+    int cycle[kMaxDims];  // per collective: cycle length side / gcd(side, distance)
     int8_t own[kMaxDims][kMaxSlots], left[kMaxDims][kMaxSlots], right[kMaxDims][kMaxSlots];
     uint32_t wg_base;
 };
@@ -735,27 +742,35 @@ template <typename T, int VEC>
 __global__ __launch_bounds__(64) void slot_step_kernel(T* __restrict__ out,
                                                       const T* __restrict__ in, SlotArgs a) {
     using V = Vec<T, VEC>;
-    const uint32_t unit = a.wg_base + blockIdx.x;
+    const uint32_t unit = a.wg_base + xcd_contiguous(blockIdx.x, gridDim.x);
     if (unit >= a.units) return;
-    const uint32_t cb = unit % a.colblocks;
-    const uint32_t rest = unit / a.colblocks;
-    const int x = (int)(rest % (uint32_t)a.n);
-    const int c = (int)(rest / (uint32_t)a.n);
+    // unit = ((c * cycles + cycle) * colblocks + cb) * L + i, i the position along the cycle
+    const uint32_t per_coll = (uint32_t)a.n * a.colblocks;
+    const int c = (int)(unit / per_coll);
+    uint32_t r = unit - (uint32_t)c * per_coll;
+    const int dim = a.act[c], side = a.side[dim], stride = a.stride[dim], dist = a.dist[c];
+    const uint32_t L = (uint32_t)a.cycle[c];
+    const int i = (int)(r % L);
+    r /= L;
+    const uint32_t cb = r % a.colblocks;
+    const int cyc = (int)(r / a.colblocks);
+    const int g = side / (int)L;  // cycles per line
+    const int line = cyc / g, res = cyc - line * g;
+    const int xa = (res + (int)(((int64_t)i * dist) % side)) % side;  // coordinate along dim
+    const int x = (line % stride) + (line / stride) * stride * side + xa * stride;
     const int64_t E = a.elems;
     const int64_t seg_b = imin64(a.seg_g[c] * kGranule, E);
     const int64_t seg_e = imin64(a.seg_g[c + 1] * kGranule, E);
     const int64_t col = seg_b + ((int64_t)cb * 64 + threadIdx.x) * VEC;
     if (col >= seg_e) return;
-    const int stride = a.stride[a.act[c]], side = a.side[a.act[c]], dist = a.dist[c];
-    const int xa = (x / stride) % side;
     const int xl = x + ((xa >= dist ? -dist : side - dist) * stride);
     const int xr = x + ((xa + dist < side ? dist : dist - side) * stride);
     const T* const own_row = in + (int64_t)x * E + col;
     const T* const left_row = in + (int64_t)xl * E + col;
     const T* const right_row = in + (int64_t)xr * E + col;
     T* const out_row = out + (int64_t)x * E + col;
-    for (int i = 0; i < a.nout[c]; ++i) {
-        const int so = a.own[c][i], sl = a.left[c][i], sr = a.right[c][i];
+    for (int k = 0; k < a.nout[c]; ++k) {
+        const int so = a.own[c][k], sl = a.left[c][k], sr = a.right[c][k];
         V acc;
         bool have = false;
         if (so >= 0) {
@@ -771,7 +786,7 @@ __global__ __launch_bounds__(64) void slot_step_kernel(T* __restrict__ out,
             const V v = ld<T, VEC>(right_row + sr * a.slot_stride);
             acc = have ? vadd(acc, v) : v;
         }
-        st<T, VEC, true>(out_row + (int64_t)i * a.slot_stride, acc);
+        st<T, VEC, true>(out_row + (int64_t)k * a.slot_stride, acc);
     }
 }
 
@@ -1166,6 +1181,13 @@ int run_slot_passes(T* buf, int64_t elems, const trivance_plan_t* p, T* ws, hipS
             a.act[c] = ps.dim[c];
             a.dist[c] = ps.distance[c];
             a.nout[c] = sp.nout[c];
+            int g = p->dims[ps.dim[c]], h = ps.distance[c];  // gcd(side, distance)
+            while (h) {
+                const int t = g % h;
+                g = h;
+                h = t;
+            }
+            a.cycle[c] = p->dims[ps.dim[c]] / g;
             for (int i = 0; i < kMaxSlots; ++i) {
                 a.own[c][i] = sp.own[c][i];
                 a.left[c][i] = sp.left[c][i];

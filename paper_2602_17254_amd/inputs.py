@@ -113,6 +113,14 @@ WORKLOADS = {
                  ("nonpower3",)),
         Workload("torus16x16x16_B_8MiB", (16, 16, 16), "B", 2_097_152, "hash_uniform", 9, None,
                  False, ("nonpower3",)),
+        # the latency-optimal variant on the paper's sides that are not powers of three (partial
+        # sums in a caller-owned workspace: 0.5, 4 and 144 GiB)
+        Workload("ring8_L_8MiB", (8,), "L", 2_097_152, "normal", 10, (-(2 ** 20), 2 ** 20), True,
+                 ("nonpower3",)),
+        Workload("ring64_L_8MiB", (64,), "L", 2_097_152, "hash_uniform", 11, None, True,
+                 ("nonpower3",)),
+        Workload("torus32x32_L_8MiB", (32, 32), "L", 2_097_152, "hash_uniform", 12, None, True,
+                 ("nonpower3",)),
         # the power-of-three bandwidth-optimal workloads with message-contiguous block placement
         # (same inputs as their default-partition counterparts)
         Workload("ring243_Bp_32MiB", (243,), "B", 8_388_608, "normal", 2, (-(2 ** 20), 2 ** 20),

@@ -185,6 +185,63 @@ def test_torus16x16x16_bandwidth_8MiB_nonpower3():
     _device_hash_workload(w, max_blocks=64)
 
 
+# The latency-optimal variant on sides that are not powers of three (partials in a workspace).
+def _run_full_ws(w, buf):
+    import paper_2602_17254_amd as T
+
+    plan = T.trivance_plan(w.dims, w.variant, w.placement)
+    ws = torch.empty(T.trivance_workspace_bytes(plan, w.elems), dtype=torch.uint8, device="cuda")
+    T.trivance_allreduce_emulated_ws(buf, plan, ws)
+    torch.cuda.synchronize()
+    del ws
+    torch.cuda.empty_cache()
+    return buf
+
+
+def test_ring8_latency_8MiB_nonpower3():
+    w = inputs.WORKLOADS["ring8_L_8MiB"]
+    _say(f"[workload] {w.name} f32 (full comparison)")
+    V = inputs.normal_f32(w.seed, w.n, w.elems)
+    buf = _run_full_ws(w, torch.from_numpy(V).cuda())
+    assert_matches_oracle(buf.cpu().numpy(), V, w.dims, w.variant, what=w.name)
+    _say(f"[workload] {w.name} i32 (full comparison)")
+    Vi = inputs.uniform_i32(w.int_seed, w.n, w.elems, *w.int_range)
+    buf = _run_full_ws(w, torch.from_numpy(Vi).cuda())
+    assert_matches_oracle(buf.cpu().numpy(), Vi, w.dims, w.variant, what=w.name)
+    _congestion(w)
+
+
+def _device_hash_latency(w):
+    import paper_2602_17254_amd as T
+
+    D = len(w.dims)
+    buf = torch.empty((w.n, w.elems), dtype=torch.float32, device="cuda")
+    T.trivance_fill_hash_uniform(buf, w.seed)
+    _run_full_ws(w, buf)
+    cols, seg, _ = sample_columns(w.elems, D, w.n, "L", w.seed)
+    got = buf.index_select(1, torch.from_numpy(cols).cuda()).cpu().numpy()
+    del buf
+    torch.cuda.empty_cache()
+    Vs = inputs.hash_uniform(w.seed, w.elems, np.arange(w.n), cols)
+    assert_matches_oracle(got, Vs, w.dims, w.variant, col_seg=seg, what=w.name)
+
+
+def test_ring64_latency_8MiB_nonpower3():
+    w = inputs.WORKLOADS["ring64_L_8MiB"]
+    _say(f"[workload] {w.name} f32, device-generated inputs (column sample)")
+    _device_hash_latency(w)
+    _congestion(w)
+
+
+def test_torus32x32_latency_8MiB_nonpower3():
+    """1024 ranks of 8 MiB with up to nine partials per rank: 8.6 GB of rank data and a 155 GB
+    workspace."""
+    w = inputs.WORKLOADS["torus32x32_L_8MiB"]
+    _say(f"[workload] {w.name} f32, device-generated inputs (column sample)")
+    _device_hash_latency(w)
+    _congestion(w)
+
+
 # The power-of-three bandwidth-optimal workloads with message-contiguous block placement: the
 # same column sample, labelled with the block placed at each column's granule range.
 def test_ring243_bandwidth_32MiB_placed():

@@ -39,7 +39,7 @@ def test_workload_table():
     w = inputs.WORKLOADS
     assert inputs.HEADLINE in w
     assert [x.n for x in w.values()] == [9, 81, 243, 729, 729, 8, 64, 1024, 512, 4096,
-                                         243, 729, 729]
+                                         8, 64, 1024, 243, 729, 729]
     placed = [x for x in w.values() if x.placement == "schedule"]
     assert [x.name for x in placed] == ["ring243_Bp_32MiB", "torus27x27_Bp_4MiB",
                                         "torus9x9x9_Bp_128MiB"]
