@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtrivance.so")
 
-HIP_SOURCES = ["executor.hip", "congestion.hip", "fill.hip"]
+HIP_SOURCES = ["executor.hip", "slot.hip", "congestion.hip", "fill.hip"]
 CXX_SOURCES = ["plan.cpp", "cost.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

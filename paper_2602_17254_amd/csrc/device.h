@@ -1,0 +1,106 @@
+// Device-side building blocks shared by the step kernels (executor.hip, slot.hip): vectors of
+// elements, 16-byte loads and stores, the joint reduction in its fixed order, and the XCD-aware
+// workgroup order.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "plan.h"
+
+namespace trivance {
+
+// x / d for x < 2^31 with the multiplier of make_fastdiv32 (plan.h).
+__device__ __forceinline__ uint32_t fdiv32(uint32_t x, FastDiv32 f) {
+    return __umulhi(x << 1, f.mul) >> f.shift;
+}
+
+template <typename T, int N>
+struct alignas(sizeof(T) * N) Vec {
+    T v[N];
+};
+
+__device__ __forceinline__ float add1(float a, float b) { return a + b; }
+__device__ __forceinline__ int add1(int a, int b) {
+    return (int)((unsigned)a + (unsigned)b);  // two's-complement wrap
+}
+
+template <typename T, int N>
+__device__ __forceinline__ Vec<T, N> vadd(const Vec<T, N>& a, const Vec<T, N>& b) {
+    Vec<T, N> r;
+#pragma unroll
+    for (int i = 0; i < N; ++i) r.v[i] = add1(a.v[i], b.v[i]);
+    return r;
+}
+
+// Joint reduction of Sec. 4.3 in the fixed order (own + left) + right.
+template <typename T, int N>
+__device__ __forceinline__ Vec<T, N> joint(const Vec<T, N>& own, const Vec<T, N>& left,
+                                           const Vec<T, N>& right) {
+    return vadd(vadd(own, left), right);
+}
+
+template <typename T, int N>
+using Native = T __attribute__((ext_vector_type(N)));
+
+// 16-byte (or element) load/store; NT selects the non-temporal (streaming) cache policy.
+template <typename T, int N, bool NT = false>
+__device__ __forceinline__ Vec<T, N> ld(const T* p) {
+    Vec<T, N> r;
+    if constexpr (N == 1) {
+        r.v[0] = NT ? __builtin_nontemporal_load(p) : *p;
+    } else {
+        const Native<T, N>* q = reinterpret_cast<const Native<T, N>*>(p);
+        const Native<T, N> x = NT ? __builtin_nontemporal_load(q) : *q;
+#pragma unroll
+        for (int i = 0; i < N; ++i) r.v[i] = x[i];
+    }
+    return r;
+}
+
+template <typename T, int N, bool NT = false>
+__device__ __forceinline__ void st(T* p, const Vec<T, N>& v) {
+    if constexpr (N == 1) {
+        if (NT) __builtin_nontemporal_store(v.v[0], p);
+        else *p = v.v[0];
+    } else {
+        Native<T, N> x;
+#pragma unroll
+        for (int i = 0; i < N; ++i) x[i] = v.v[i];
+        Native<T, N>* q = reinterpret_cast<Native<T, N>*>(p);
+        if (NT) __builtin_nontemporal_store(x, q);
+        else *q = x;
+    }
+}
+
+__device__ __forceinline__ int64_t imin64(int64_t a, int64_t b) { return a < b ? a : b; }
+
+// Workgroup index remapped so that each of the 8 XCDs (which receive workgroups round-robin)
+// works on one contiguous range of units.
+__device__ __forceinline__ uint32_t xcd_contiguous(uint32_t wg, uint32_t nwg) {
+    constexpr uint32_t kXcds = 8;
+    const uint32_t per = nwg / kXcds, rem = nwg % kXcds;
+    const uint32_t xcd = wg % kXcds, idx = wg / kXcds;
+    return xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+}
+
+
+
+// Where and how a call's launches go: the stream, and the most work-items of one dispatch (the
+// plan's limit).
+struct Exec {
+    hipStream_t stream;
+    int64_t items;
+};
+
+
+// Latency-optimal passes on sides that are not powers of three (slot.hip): the workspace halves a
+// slot plan uses, and the launcher of passes [pb, pe).
+int slot_halves(const trivance_plan_t* p);
+int run_slot_passes(float* buf, int64_t elems, const trivance_plan_t* p, float* ws,
+                    hipStream_t stream, int pb, int pe);
+int run_slot_passes(int* buf, int64_t elems, const trivance_plan_t* p, int* ws, hipStream_t stream,
+                    int pb, int pe);
+
+}  // namespace trivance

@@ -33,6 +33,7 @@
 #include <cstdint>
 #include <cstring>
 
+#include "device.h"
 #include "plan.h"
 
 namespace trivance {
@@ -96,76 +97,6 @@ struct StepArgs {
                                                      // word i / 4; entry pexp_off[d] + k is the
                                                      // position exponent of digit k of dimension d
 };
-
-template <typename T, int N>
-struct alignas(sizeof(T) * N) Vec {
-    T v[N];
-};
-
-__device__ __forceinline__ float add1(float a, float b) { return a + b; }
-__device__ __forceinline__ int add1(int a, int b) {
-    return (int)((unsigned)a + (unsigned)b);  // two's-complement wrap
-}
-
-template <typename T, int N>
-__device__ __forceinline__ Vec<T, N> vadd(const Vec<T, N>& a, const Vec<T, N>& b) {
-    Vec<T, N> r;
-#pragma unroll
-    for (int i = 0; i < N; ++i) r.v[i] = add1(a.v[i], b.v[i]);
-    return r;
-}
-
-// Joint reduction of Sec. 4.3 in the fixed order (own + left) + right.
-template <typename T, int N>
-__device__ __forceinline__ Vec<T, N> joint(const Vec<T, N>& own, const Vec<T, N>& left,
-                                           const Vec<T, N>& right) {
-    return vadd(vadd(own, left), right);
-}
-
-template <typename T, int N>
-using Native = T __attribute__((ext_vector_type(N)));
-
-// 16-byte (or element) load/store; NT selects the non-temporal (streaming) cache policy.
-template <typename T, int N, bool NT = false>
-__device__ __forceinline__ Vec<T, N> ld(const T* p) {
-    Vec<T, N> r;
-    if constexpr (N == 1) {
-        r.v[0] = NT ? __builtin_nontemporal_load(p) : *p;
-    } else {
-        const Native<T, N>* q = reinterpret_cast<const Native<T, N>*>(p);
-        const Native<T, N> x = NT ? __builtin_nontemporal_load(q) : *q;
-#pragma unroll
-        for (int i = 0; i < N; ++i) r.v[i] = x[i];
-    }
-    return r;
-}
-
-template <typename T, int N, bool NT = false>
-__device__ __forceinline__ void st(T* p, const Vec<T, N>& v) {
-    if constexpr (N == 1) {
-        if (NT) __builtin_nontemporal_store(v.v[0], p);
-        else *p = v.v[0];
-    } else {
-        Native<T, N> x;
-#pragma unroll
-        for (int i = 0; i < N; ++i) x[i] = v.v[i];
-        Native<T, N>* q = reinterpret_cast<Native<T, N>*>(p);
-        if (NT) __builtin_nontemporal_store(x, q);
-        else *q = x;
-    }
-}
-
-__device__ __forceinline__ int64_t imin64(int64_t a, int64_t b) { return a < b ? a : b; }
-
-// Workgroup index remapped so that each of the 8 XCDs (which receive workgroups round-robin)
-// works on one contiguous range of units.
-__device__ __forceinline__ uint32_t xcd_contiguous(uint32_t wg, uint32_t nwg) {
-    constexpr uint32_t kXcds = 8;
-    const uint32_t per = nwg / kXcds, rem = nwg % kXcds;
-    const uint32_t xcd = wg % kXcds, idx = wg / kXcds;
-    return xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
-}
-
 
 // ---------------------------------------------------------------------------------------------
 // Latency-optimal step: sliding window over one rank cycle.
@@ -525,9 +456,6 @@ struct TreeArgs {
 static_assert(sizeof(TreeArgs<kMaxTreeDims, kMaxTab>) <= 4096,
               "tree-step kernel arguments above 4 KiB");
 
-__device__ __forceinline__ uint32_t fdiv32(uint32_t x, FastDiv32 f) {
-    return __umulhi(x << 1, f.mul) >> f.shift;
-}
 
 // One decoded unit (wave-uniform) and the state its successors are derived from.
 struct TreeUnit {
@@ -710,95 +638,7 @@ __global__ __launch_bounds__(64) void tree_step_kernel(T* __restrict__ buf, Tree
 }
 
 // ---------------------------------------------------------------------------------------------
-// Latency-optimal step on sides that are not powers of three (Sec. 4.2 with Sec. 4.4): every rank
-// keeps a few partial sums ("slots", see plan.cpp) per collective. Output slot i of rank x is the
-// joint reduction (own + left) + right of input slot own[i] of x, left[i] of the peer at -distance
-// and right[i] of the peer at +distance along the collective's active dimension (absent terms
-// skipped). Inputs and outputs are different state arrays (slot s of a state is an [n][elems]
-// array at s * n * elems), so the pass has no in-place hazard.
-//
-// One wave handles 64 column vectors of one rank of one collective and computes all its output
-// slots. Along the active dimension the ranks x, x + d, x + 2d, ... form cycles; units are
-// numbered so that consecutive ones are consecutive ranks of one cycle at the same columns, and
-// each XCD takes one contiguous range of units: the partials a wave reads from its peers at -d
-// and +d were just read by its neighbours in the schedule, so they come from the XCD's L2 rather
-// than HBM.
-struct SlotArgs {
-    int64_t elems;
-    int64_t seg_g[kMaxDims + 1];
-    int64_t slot_stride;  // elements from one slot array to the next: n * elems
-    int n;
-    int D;
-    uint32_t colblocks;   // column blocks of 64 vectors per rank (largest segment)
-    uint32_t units;       // D * n * colblocks
-    int act[kMaxDims], dist[kMaxDims], side[kMaxDims], stride[kMaxDims], nout[kMaxDims];
-    int cycle[kMaxDims];  // per collective: cycle length side / gcd(side, distance)
-    int8_t own[kMaxDims][kMaxSlots], left[kMaxDims][kMaxSlots], right[kMaxDims][kMaxSlots];
-    uint32_t wg_base;
-};
-static_assert(sizeof(SlotArgs) <= 4096, "slot-step kernel arguments above 4 KiB");
-
-template <typename T, int VEC>
-__global__ __launch_bounds__(64) void slot_step_kernel(T* __restrict__ out,
-                                                      const T* __restrict__ in, SlotArgs a) {
-    using V = Vec<T, VEC>;
-    const uint32_t unit = a.wg_base + xcd_contiguous(blockIdx.x, gridDim.x);
-    if (unit >= a.units) return;
-    // unit = ((c * cycles + cycle) * colblocks + cb) * L + i, i the position along the cycle
-    const uint32_t per_coll = (uint32_t)a.n * a.colblocks;
-    const int c = (int)(unit / per_coll);
-    uint32_t r = unit - (uint32_t)c * per_coll;
-    const int dim = a.act[c], side = a.side[dim], stride = a.stride[dim], dist = a.dist[c];
-    const uint32_t L = (uint32_t)a.cycle[c];
-    const int i = (int)(r % L);
-    r /= L;
-    const uint32_t cb = r % a.colblocks;
-    const int cyc = (int)(r / a.colblocks);
-    const int g = side / (int)L;  // cycles per line
-    const int line = cyc / g, res = cyc - line * g;
-    const int xa = (res + (int)(((int64_t)i * dist) % side)) % side;  // coordinate along dim
-    const int x = (line % stride) + (line / stride) * stride * side + xa * stride;
-    const int64_t E = a.elems;
-    const int64_t seg_b = imin64(a.seg_g[c] * kGranule, E);
-    const int64_t seg_e = imin64(a.seg_g[c + 1] * kGranule, E);
-    const int64_t col = seg_b + ((int64_t)cb * 64 + threadIdx.x) * VEC;
-    if (col >= seg_e) return;
-    const int xl = x + ((xa >= dist ? -dist : side - dist) * stride);
-    const int xr = x + ((xa + dist < side ? dist : dist - side) * stride);
-    const T* const own_row = in + (int64_t)x * E + col;
-    const T* const left_row = in + (int64_t)xl * E + col;
-    const T* const right_row = in + (int64_t)xr * E + col;
-    T* const out_row = out + (int64_t)x * E + col;
-    for (int k = 0; k < a.nout[c]; ++k) {
-        const int so = a.own[c][k], sl = a.left[c][k], sr = a.right[c][k];
-        V acc;
-        bool have = false;
-        if (so >= 0) {
-            acc = ld<T, VEC>(own_row + so * a.slot_stride);
-            have = true;
-        }
-        if (sl >= 0) {
-            const V v = ld<T, VEC>(left_row + sl * a.slot_stride);
-            acc = have ? vadd(acc, v) : v;
-            have = true;
-        }
-        if (sr >= 0) {
-            const V v = ld<T, VEC>(right_row + sr * a.slot_stride);
-            acc = have ? vadd(acc, v) : v;
-        }
-        st<T, VEC, true>(out_row + (int64_t)k * a.slot_stride, acc);
-    }
-}
-
-// ---------------------------------------------------------------------------------------------
 // Host side.
-
-// Where and how a call's launches go: the stream, and the most work-items of one dispatch (the
-// plan's limit).
-struct Exec {
-    hipStream_t stream;
-    int64_t items;
-};
 
 // Enqueues `kernel` over `grid` workgroups of `threads` work-items as consecutive dispatches of
 // whole workgroups (for_each_dispatch), each with its first workgroup in the argument block.
@@ -1147,83 +987,10 @@ int run_tree_passes(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t
     }
 }
 
-// Workspace halves of a slot plan: state t (0 < t < S) lives in half (t - 1) % 2; a one-pass plan
-// writes its result to half 0 and copies it back (input and output must not alias).
-inline int slot_halves(const trivance_plan_t* p) { return p->S >= 3 ? 2 : (p->S >= 1 ? 1 : 0); }
-
-template <typename T, int VEC>
-int run_slot_passes(T* buf, int64_t elems, const trivance_plan_t* p, T* ws, hipStream_t stream,
-                    int pb, int pe) {
-    const Exec x{stream, p->dispatch_items};
-    SlotArgs a;
-    std::memset(&a, 0, sizeof(a));
-    a.elems = elems;
-    a.n = p->n;
-    a.D = p->D;
-    a.slot_stride = (int64_t)p->n * elems;
-    const int64_t G = (elems + kGranule - 1) / kGranule;
-    int64_t max_seg = 0;
-    for (int c = 0; c <= p->D; ++c) a.seg_g[c] = (int64_t)c * G / p->D;
-    for (int c = 0; c < p->D; ++c)
-        max_seg = std::max(max_seg, std::min(a.seg_g[c + 1] * kGranule, elems) -
-                                        std::min(a.seg_g[c] * kGranule, elems));
-    const int64_t vecs = (max_seg + VEC - 1) / VEC;
-    a.colblocks = (uint32_t)std::max<int64_t>(1, (vecs + 63) / 64);
-    const int64_t units = (int64_t)p->D * p->n * a.colblocks;
-    if (units >= ((int64_t)1 << 31)) return TRIVANCE_EUNSUPPORTED;
-    a.units = (uint32_t)units;
-    const int64_t half = (int64_t)p->max_slots * a.slot_stride;
-    const int S = p->S;
-    for (int pi = pb; pi < pe; ++pi) {
-        const Pass& ps = p->passes[pi];
-        const SlotPass& sp = p->slots[pi];
-        for (int c = 0; c < p->D; ++c) {
-            a.act[c] = ps.dim[c];
-            a.dist[c] = ps.distance[c];
-            a.nout[c] = sp.nout[c];
-            int g = p->dims[ps.dim[c]], h = ps.distance[c];  // gcd(side, distance)
-            while (h) {
-                const int t = g % h;
-                g = h;
-                h = t;
-            }
-            a.cycle[c] = p->dims[ps.dim[c]] / g;
-            for (int i = 0; i < kMaxSlots; ++i) {
-                a.own[c][i] = sp.own[c][i];
-                a.left[c][i] = sp.left[c][i];
-                a.right[c][i] = sp.right[c][i];
-            }
-        }
-        for (int d = 0; d < kMaxDims; ++d) {
-            a.side[d] = d < p->D ? p->dims[d] : 1;
-            a.stride[d] = d < p->D ? p->strides[d] : 1;
-        }
-        const T* in = pi == 0 ? buf : ws + ((pi - 1) % 2) * half;
-        T* out = (pi == S - 1 && S > 1) ? buf : ws + (pi % 2) * half;
-        hipError_t err = hipSuccess;
-        for_each_dispatch(a.units, 64, x.items, [&](uint32_t first, uint32_t count) {
-            a.wg_base = first;
-            hipLaunchKernelGGL((slot_step_kernel<T, VEC>), dim3(count), dim3(64), 0, x.stream, out,
-                               in, a);
-            err = hipGetLastError();
-            return err == hipSuccess;
-        });
-        if (err != hipSuccess) return TRIVANCE_EHIP;
-        if (S == 1 && hipMemcpyAsync(buf, ws, (size_t)a.slot_stride * sizeof(T),
-                                     hipMemcpyDeviceToDevice, stream) != hipSuccess)
-            return TRIVANCE_EHIP;
-    }
-    return TRIVANCE_OK;
-}
-
 template <typename T>
 int run_passes(T* buf, int64_t elems, const trivance_plan_t* p, T* ws, hipStream_t stream, int pb,
                int pe) {
-    if (!p->slots.empty()) {
-        if (elems % 4 == 0 && (uintptr_t)buf % 16 == 0 && (uintptr_t)ws % 16 == 0)
-            return run_slot_passes<T, 4>(buf, elems, p, ws, stream, pb, pe);
-        return run_slot_passes<T, 1>(buf, elems, p, ws, stream, pb, pe);
-    }
+    if (!p->slots.empty()) return run_slot_passes(buf, elems, p, ws, stream, pb, pe);
     if (p->tree) {
         if (elems % 4 == 0 && (uintptr_t)buf % 16 == 0)
             return run_tree_passes<T, 4>(buf, elems, p, stream, pb, pe);
