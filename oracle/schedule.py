@@ -124,13 +124,25 @@ def peers_ring(r: int, k: int, n: int) -> tuple:
     return (r - 3 ** k) % n, (r + 3 ** k) % n
 
 
-def reach(torus: Torus, c: int, p: int, t: int) -> frozenset:
-    """Ranks that data held by p must still be forwarded to, from global step t onwards.
+def remaining_reach(torus: Torus, c: int, p: int, t: int) -> frozenset:
+    """Ranks (p included) that data held by p can still travel to in global steps t .. S-1.
 
-    This is the forward-reachability map of Algorithm 1 (BlockPropagation): from p, every later
-    step contacts both peers, and every contacted rank continues from the following step. The
-    ring version of the paper is the D = 1 case; for tori the per-collective step list above is
-    used. p itself is never marked (the algorithm only marks peers)."""
+    Each remaining step may move a partial by -d, 0 or +d along that step's dimension and distance
+    (Sec. 4.1: every rank exchanges with both peers and every partial moves at most once per step),
+    so the set grows step by step: everything reached so far, shifted by each of the three moves.
+    This is the reachability that Algorithm 1 (BlockPropagation) computes recursively; `reach` below
+    transcribes that algorithm, and the tests check that both agree."""
+    cur = {p}
+    for t2 in range(t, torus.steps):
+        dim, dist = step_dim_and_distance(torus, c, t2)
+        cur = {torus.shift(x, dim, e * dist) for x in cur for e in (-1, 0, +1)}
+    return frozenset(cur)
+
+
+def reach(torus: Torus, c: int, p: int, t: int) -> frozenset:
+    """Algorithm 1 (BlockPropagation) as printed, generalised to the torus step list: from p, every
+    later step contacts both peers, and every contacted rank continues from the following step. p
+    itself is never marked (the algorithm only marks peers). A cross-check of remaining_reach."""
     return _reach_cached(torus, c, p, t)
 
 
@@ -144,14 +156,19 @@ def _reach_cached(torus: Torus, c: int, p: int, t: int) -> frozenset:
     return frozenset(marked)
 
 
+@lru_cache(maxsize=None)
+def _message_cached(torus: Torus, c: int, receiver: int, t: int) -> tuple:
+    return tuple(sorted(remaining_reach(torus, c, receiver, t + 1)))
+
+
 def message_blocks(torus: Torus, c: int, receiver: int, t: int) -> list:
     """Blocks a rank sends to `receiver` at reduce-scatter step t (Sec. 4.1, 4.3).
 
     The sender forwards the block destined for the receiver plus the blocks of every node the
-    receiver will reach in the remaining steps. Reading: Algorithm 1 does not mark its start node,
-    so the receiver's own block is added explicitly. The set does not depend on which side sends.
-    Returned sorted, which also fixes the order of the values inside a message."""
-    return sorted({receiver} | set(reach(torus, c, receiver, t + 1)))
+    receiver will reach in the remaining steps t+1 .. S-1 (remaining_reach, which includes the
+    receiver itself). The set does not depend on which side sends. Returned sorted, which also
+    fixes the order of the values inside a message."""
+    return list(_message_cached(torus, c, receiver, t))
 
 
 def pi_closed_form_ring(n: int, p: int, k: int) -> list:

@@ -45,8 +45,9 @@ def test_ring_peers_are_pm_3k():
 
 @pytest.mark.parametrize("n", RINGS)
 def test_algorithm1_matches_closed_form(n):
-    """Sec. 4.3: the recursive BlockPropagation and the closed form Pi(n, r, p, k) agree, and a
-    message at step k carries 3^(s-1-k) blocks."""
+    """Sec. 4.3: the message blocks (the step-by-step reachability), Algorithm 1's recursive
+    BlockPropagation (plus the receiver it never marks) and the closed form Pi(n, r, p, k) are
+    the same sets, and a message at step k carries 3^(s-1-k) blocks."""
     t = schedule.Torus((n,))
     s = t.steps
     for k in range(s):
@@ -54,7 +55,20 @@ def test_algorithm1_matches_closed_form(n):
             for p in schedule.peers(t, 0, r, k):
                 blocks = schedule.message_blocks(t, 0, p, k)
                 assert blocks == schedule.pi_closed_form_ring(n, p, k)
+                assert blocks == sorted({p} | set(schedule.reach(t, 0, p, k + 1)))
                 assert len(blocks) == 3 ** (s - 1 - k)
+
+
+@pytest.mark.parametrize("dims", [(3, 3), (9, 9), (3, 3, 3), (3, 9), (9, 3, 3), (27, 3)])
+def test_algorithm1_matches_reachability_on_tori(dims):
+    """On tori (Sec. 5) the step-by-step reachability and Algorithm 1 over the collective's step
+    list give the same block sets for every collective, receiver and step."""
+    t = schedule.Torus(dims)
+    for c in range(t.D):
+        for k in range(t.steps):
+            for p in range(t.n):
+                assert schedule.message_blocks(t, c, p, k) == \
+                    sorted({p} | set(schedule.reach(t, c, p, k + 1)))
 
 
 def test_n9_golden_message_sizes():
