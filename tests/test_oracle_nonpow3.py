@@ -269,6 +269,26 @@ def test_torus_gather_form_equals_mailbox_form(dims, dtype):
                                   nonpow3.link_loads_torus(dims, "mailbox"))
 
 
+@pytest.mark.parametrize("dims", [(8, 8), (10, 10), (16, 16), (8, 16), (5, 5, 5), (6, 6, 6),
+                                  (350,)], ids=lambda d: "x".join(map(str, d)))
+def test_gather_form_equals_mailbox_form_on_larger_shapes(dims):
+    """The same pin on the shapes between the small ones above and the 1024- and 4096-rank
+    workloads the gather form checks alone (and on a ring above the 300 ranks where the GPU tests
+    switch to it): one column per block, so every partial of every block is compared."""
+    n = int(np.prod(dims))
+    D = len(dims)
+    seg = np.repeat(np.arange(D), n)
+    blk = np.tile(np.arange(n), D)
+    V = (np.random.default_rng(n + D).standard_normal((n, D * n)) *
+         np.logspace(-4, 4, D * n)).astype(np.float32)
+    a = nonpow3.bandwidth_optimal_torus_columns(V, dims, seg, blk)
+    if D == 1:
+        b = nonpow3.bandwidth_optimal_ring(V, col_blk=blk)
+    else:
+        b = nonpow3.bandwidth_optimal_torus(V, dims, seg, blk)
+    np.testing.assert_array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
 def test_rectangular_tree_torus_final_steps_share_the_long_dimension():
     """8 x 64 under the rotation rule for unequal step counts: the side of 8 is done after two
     steps of each collective, so both collectives take the last two steps of the side of 64
