@@ -39,34 +39,18 @@ METRIC = "emulated AllReduce HBM GB/s and % of HBM peak, per-rank 8-128 MiB, 1 G
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 
 # HBM traffic per launch measured with rocprofv3 --pmc (FETCH_SIZE / WRITE_SIZE, scaled by the
-# same counters read for a plain copy of known size), keyed by kernel, valid only for the kernel
-# source it was measured on (sha256 of the source file, first 16 hex digits).
+# same counters read for a plain copy of known size), keyed by workload and kernel, valid only for
+# the kernel source it was measured on (sha256 of that source file, first 16 hex digits); the
+# summaries are profiles/<kernel>_<workload>.md.
 MEASURED_TRAFFIC = {
-    # profiles/<kernel>_<workload>.md
-    ("ring81_L_8MiB", "latency_split_kernel"): {"src_sha": "a788f015396fac01",
-        "bytes_per_launch": 1359169888},
-    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
-        "bytes_per_launch": 3248091467},
-    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
-        "bytes_per_launch": 1017891728},
-    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
-        "bytes_per_launch": 32569532382},
-    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
-        "bytes_per_launch": 251703483},
-    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
-        "bytes_per_launch": 283160224},
-    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
-        "bytes_per_launch": 2286956084},
-    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
-        "bytes_per_launch": 1550517906},
-    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
-        "bytes_per_launch": 9724117915},
-    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
-        "bytes_per_launch": 3248094104},
-    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
-        "bytes_per_launch": 1017897153},
-    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {"src_sha": "a788f015396fac01",
-        "bytes_per_launch": 32569664182},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {
+        "src": "executor.hip", "src_sha": "3bf66eadd0819c3d", "bytes_per_launch": 32568980173},
+    ("torus9x9x9_B_128MiB", "block_step_kernel<copy>"): {
+        "src": "executor.hip", "src_sha": "3bf66eadd0819c3d", "bytes_per_launch": 24427305497},
+    ("ring64_L_8MiB", "slot_step_kernel"): {
+        "src": "slot.hip", "src_sha": "600954b1aa4af192", "bytes_per_launch": 3234234582},
+    ("torus32x32_L_8MiB", "slot_step_kernel"): {
+        "src": "slot.hip", "src_sha": "600954b1aa4af192", "bytes_per_launch": 96405315644},
 }
 
 
@@ -350,11 +334,11 @@ def run_workload(w, steps, warmup, with_cpu, dtype="f32"):
     dom_ms = float(group_ms[:, dg].mean()) / launches
     dom_bytes = sum(pass_bytes[pb:pe]) / launches
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    src = os.path.join(ROOT, "paper_2602_17254_amd", "csrc", "executor.hip")
     # counters were taken on the fp32 runs
     meas = MEASURED_TRAFFIC.get((w.name, names[dom])) if dtype == "f32" else None
     traffic = None
-    if meas and meas["src_sha"] == _src_sha(src):
+    if meas and meas["src_sha"] == _src_sha(os.path.join(ROOT, "paper_2602_17254_amd", "csrc",
+                                                          meas["src"])):
         traffic = meas["bytes_per_launch"]
     roofline = {
         "bound": "hbm",
