@@ -48,9 +48,9 @@ MEASURED_TRAFFIC = {
     ("torus9x9x9_B_128MiB", "block_step_kernel<copy>"): {
         "src": "executor.hip", "src_sha": "3bf66eadd0819c3d", "bytes_per_launch": 24427305497},
     ("ring64_L_8MiB", "slot_step_kernel"): {
-        "src": "slot.hip", "src_sha": "600954b1aa4af192", "bytes_per_launch": 3234234582},
+        "src": "slot.hip", "src_sha": "1079e8e55be99701", "bytes_per_launch": 3238169255},
     ("torus32x32_L_8MiB", "slot_step_kernel"): {
-        "src": "slot.hip", "src_sha": "600954b1aa4af192", "bytes_per_launch": 96405315644},
+        "src": "slot.hip", "src_sha": "1079e8e55be99701", "bytes_per_launch": 96740133890},
 }
 
 
