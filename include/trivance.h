@@ -244,8 +244,10 @@ int64_t trivance_workspace_bytes(const trivance_plan_t* plan, int64_t elems, int
  * fine for plans that need none). The workspace holds the partial sums between passes (Sec. 4.4,
  * latency-optimal: see trivance_plan); its contents on entry do not matter and are left
  * undefined. A 16-byte aligned workspace keeps the 16-byte vector path. Calls that share a
- * workspace or buffers race. Errors: those of trivance_allreduce_emulated, and ESIZE for a
- * workspace below the required size.
+ * workspace or buffers race. Like the plain form it enqueues kernel launches only (a one-pass
+ * program copies its result back with a kernel), so it can be captured into a HIP graph.
+ * Errors: those of trivance_allreduce_emulated, and ESIZE for a workspace below the required
+ * size.
  */
 int trivance_allreduce_emulated_ws(void* buffers, int n, int64_t elems, int dtype,
                                    const trivance_plan_t* plan, void* workspace,

@@ -136,6 +136,15 @@ __global__ __launch_bounds__(64 * kSlotWaves) void slot_step_kernel(T* __restric
         }
     }}
 
+// dst[i] = src[i] for `vecs` vectors of VEC elements (workgroups from `wg0` on).
+template <typename T, int VEC>
+__global__ __launch_bounds__(256) void copy_rows_kernel(T* __restrict__ dst,
+                                                        const T* __restrict__ src, int64_t vecs,
+                                                        uint64_t wg0) {
+    const int64_t i = (int64_t)((wg0 + blockIdx.x) * 256 + threadIdx.x);
+    if (i < vecs) st<T, VEC, true>(dst + i * VEC, ld<T, VEC, true>(src + i * VEC));
+}
+
 template <typename T, int VEC>
 int run_slot_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, T* ws, hipStream_t stream,
                     int pb, int pe) {
@@ -204,9 +213,19 @@ int run_slot_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, T* ws, 
             return err == hipSuccess;
         });
         if (err != hipSuccess) return TRIVANCE_EHIP;
-        if (S == 1 && hipMemcpyAsync(buf, ws, (size_t)a.slot_stride * sizeof(T),
-                                     hipMemcpyDeviceToDevice, stream) != hipSuccess)
-            return TRIVANCE_EHIP;
+        if (S == 1) {
+            // the one pass wrote its result to half 0: copy it back with a kernel (no runtime
+            // copy, so that the whole call is kernel launches, also under stream capture)
+            const int64_t vecs = a.slot_stride / VEC;  // slot_stride = n * elems, VEC | elems
+            for_each_dispatch(((uint64_t)vecs + 255) / 256, 256, x.items,
+                              [&](uint32_t first, uint32_t count) {
+                hipLaunchKernelGGL((copy_rows_kernel<T, VEC>), dim3(count), dim3(256), 0,
+                                   x.stream, buf, ws, vecs, (uint64_t)first);
+                err = hipGetLastError();
+                return err == hipSuccess;
+            });
+            if (err != hipSuccess) return TRIVANCE_EHIP;
+        }
     }
     return TRIVANCE_OK;
 }
