@@ -48,9 +48,9 @@ MEASURED_TRAFFIC = {
     ("torus9x9x9_B_128MiB", "block_step_kernel<copy>"): {
         "src": "executor.hip", "src_sha": "3bf66eadd0819c3d", "bytes_per_launch": 24427305497},
     ("ring64_L_8MiB", "slot_step_kernel"): {
-        "src": "slot.hip", "src_sha": "1079e8e55be99701", "bytes_per_launch": 3238169255},
+        "src": "slot.hip", "src_sha": "11314407f370ee7a", "bytes_per_launch": 3238129193},
     ("torus32x32_L_8MiB", "slot_step_kernel"): {
-        "src": "slot.hip", "src_sha": "1079e8e55be99701", "bytes_per_launch": 96740133890},
+        "src": "slot.hip", "src_sha": "11314407f370ee7a", "bytes_per_launch": 96724165064},
 }
 
 
