@@ -28,6 +28,7 @@ import os
 import shutil
 import subprocess
 
+import numpy as np
 import pytest
 
 from oracle import nonpow3
@@ -149,12 +150,14 @@ def plan_trees(sides, tmp):
         w = line.split()
         if w[0] == "tree":
             side, dist = int(w[1]), [int(x) for x in w[3:]]
-            out[side] = {"dist": dist, "tree": {}, "alive": {}}
+            out[side] = {"dist": dist, "tree": {}, "alive": {}, "recv": {}}
         elif w[0] == "recv":
             k = int(w[1])
+            out[side]["recv"][k] = {}
             for item in w[2:]:
                 o, fl = item.split(":")
                 o = int(o)
+                out[side]["recv"][k][o] = fl
                 if "L" in fl:  # the child at o - d moves towards + onto o
                     out[side]["tree"][(o - dist[k]) % side] = (k, o)
                 if "R" in fl:
@@ -170,6 +173,29 @@ def plans(tmp_path_factory):
         pytest.skip("g++ not found")
     tmp = str(tmp_path_factory.mktemp("trees"))
     return plan_trees(list(range(2, 201)) + [728, 2200], tmp)
+
+
+def tree_sum(V0, recv, dist):
+    """Block 0's value at its owner, evaluated directly from a tree: a rank starts from its own
+    contribution and, at every step at which it receives, adds the partial of the child on its
+    left (the rank at -distance) and then that of the child on its right, absent ones skipped
+    (Sec. 4.3's joint reduction); a child's partial is what it holds after its own earlier steps.
+    fp32, IEEE round to nearest. V0: the (n, m) inputs of the block's columns."""
+    n = V0.shape[0]
+
+    def value(o, upto):
+        v = V0[o].copy()
+        for k in range(upto):
+            fl = recv[k].get(o)
+            if fl is None:
+                continue
+            if "L" in fl:
+                v = v + value((o - dist[k]) % n, k)
+            if "R" in fl:
+                v = v + value((o + dist[k]) % n, k)
+        return v
+
+    return value(0, len(dist))
 
 
 SMALL = [n for n in range(2, 28) if _steps(n)[1] != 0]
@@ -310,3 +336,30 @@ def test_n32_owner_holds_15_of_32_before_the_final_step():
     assert len(held) == 15 and held < window(n)
     final_senders = {o for o, (k, _) in mine.items() if k == f}
     assert final_senders == {d, n - d}
+
+
+# sizes where no distance equals n / 2 (there a child's side is a matter of naming only)
+TREE_SUM_SIZES = [4, 5, 7, 8, 10, 11, 13, 14, 16, 20, 22, 23, 28, 32, 40, 50, 64, 80, 100, 128, 200]
+
+
+@pytest.mark.parametrize("n", TREE_SUM_SIZES)
+def test_oracle_arithmetic_is_the_plan_trees_sum(n, plans):
+    """The oracle's fp32 results on rings whose size is not a power of three equal, bit for bit,
+    block 0's sum evaluated directly from the plan's own tree tables (tree_sum above, code that
+    shares nothing with the oracle's mailbox emulation). With every column labelled block 0 the
+    bandwidth-optimal result on every rank is that sum. Inputs span twelve orders of magnitude so
+    that any other association or side order would change bits."""
+    _, _, dist = _steps(n)
+    assert all((2 * d) % n for d in dist)
+    p = plans[n]
+    E = 96
+    V = (np.random.default_rng(1000 + n).standard_normal((n, E)) *
+         np.logspace(-6, 6, E)[None, :] * np.logspace(-3, 3, n)[:, None]).astype(np.float32)
+    want = tree_sum(V, p["recv"], p["dist"])
+    got = nonpow3.bandwidth_optimal_ring(V, col_blk=np.zeros(E, dtype=np.int64))
+    for r in range(n):
+        assert np.array_equal(got[r].view(np.uint32), want.view(np.uint32)), r
+    naive = V[0].copy()
+    for u in range(1, n):
+        naive = naive + V[u]
+    assert not np.array_equal(naive.view(np.uint32), want.view(np.uint32))
