@@ -363,3 +363,73 @@ def test_oracle_arithmetic_is_the_plan_trees_sum(n, plans):
     for u in range(1, n):
         naive = naive + V[u]
     assert not np.array_equal(naive.view(np.uint32), want.view(np.uint32))
+
+
+TORUS_SUM = [(4, 4), (5, 7), (3, 8), (8, 3), (2, 3, 4), (8, 8), (10, 3, 3), (4, 4, 4), (2, 2, 2, 2)]
+
+
+def torus_sum(V0, dims, steps, recv, dist):
+    """Block 0's value at its owner on a torus, evaluated directly: steps[t] = (dimension, level)
+    of collective c's step t (the plan's rotation); recv[side] / dist[side] the plan's tree of a
+    side. A rank holding the block's partial receives, at a step along dimension a, from the
+    children its offset along a has at that level in a's tree (left before right); dimension 0
+    is the fastest-varying coordinate."""
+    n = V0.shape[0]
+    D = len(dims)
+    stride = [1] * D
+    for d in range(1, D):
+        stride[d] = stride[d - 1] * dims[d - 1]
+
+    def move(x, a, delta):
+        xa = (x // stride[a]) % dims[a]
+        return x + (((xa + delta) % dims[a]) - xa) * stride[a]
+
+    def value(x, upto):
+        v = V0[x].copy()
+        for t in range(upto):
+            a, k = steps[t]
+            side = dims[a]
+            fl = recv[side][k].get((x // stride[a]) % side)
+            if fl is None:
+                continue
+            if "L" in fl:
+                v = v + value(move(x, a, -dist[side][k]), t)
+            if "R" in fl:
+                v = v + value(move(x, a, +dist[side][k]), t)
+        return v
+
+    return value(0, len(steps))
+
+
+@pytest.mark.parametrize("dims", TORUS_SUM, ids=lambda d: "x".join(map(str, d)))
+def test_torus_oracle_arithmetic_is_the_plan_trees_sum(dims, tmp_path):
+    """The torus form: for every collective, the oracle's fp32 result (mailbox emulation, and the
+    gather form used for large tori) equals, bit for bit, block 0's sum evaluated from the plan's
+    per-side trees in the order of the plan's rotation (trivance_plan_step)."""
+    T = pytest.importorskip("paper_2602_17254_amd")
+    if shutil.which("g++") is None:
+        pytest.skip("g++ not found")
+    sides = sorted(set(dims) - {1})
+    trees = plan_trees(sides, str(tmp_path))
+    plan = T.trivance_plan(dims, "B")
+    D, n = len(dims), int(np.prod(dims))
+    E = 96
+    V = (np.random.default_rng(7 * n + D).standard_normal((n, E)) *
+         np.logspace(-6, 6, E)[None, :] * np.logspace(-3, 3, n)[:, None]).astype(np.float32)
+    recv = {s: trees[s]["recv"] for s in sides}
+    dist = {s: trees[s]["dist"] for s in sides}
+    for c in range(D):
+        level = [0] * D
+        steps = []
+        for t in range(plan.num_steps):
+            _, a, d = T.trivance_plan_step(plan, t, c)
+            assert d == dist[dims[a]][level[a]]
+            steps.append((a, level[a]))
+            level[a] += 1
+        want = torus_sum(V, dims, steps, recv, dist)
+        seg = np.full(E, c, dtype=np.int64)
+        blk = np.zeros(E, dtype=np.int64)
+        for got in (nonpow3.bandwidth_optimal_torus(V, dims, col_seg=seg, col_blk=blk),
+                    nonpow3.bandwidth_optimal_torus_columns(V, dims, seg, blk)):
+            for r in range(n):
+                assert np.array_equal(got[r].view(np.uint32), want.view(np.uint32)), (c, r)
