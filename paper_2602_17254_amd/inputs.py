@@ -63,6 +63,8 @@ class Workload:
     dist      'normal' (N(0,1) fp32 from numpy) or 'hash_uniform' (U(-1,1), generated on device)
     seed      seed of the fp32 input
     int_range inclusive int32 range of the bit-exact integer companion run, or None
+    congestion whether the bench line also reports the plan's per-link message counts checked
+              against the oracle's link walk (congestion_exact)
     placement 'natural' (block j at the j-th granule range) or 'schedule' (blocks placed by the
               digits the schedule fixes, TRIVANCE_PLACE_BY_SCHEDULE)
     """
@@ -99,9 +101,11 @@ WORKLOADS = {
     for w in [
         Workload("ring9_L_4KiB", (9,), "L", 1024, "normal", 0, (-1000, 1000), True),
         Workload("ring81_L_8MiB", (81,), "L", 2_097_152, "normal", 1, None, True),
-        Workload("ring243_B_32MiB", (243,), "B", 8_388_608, "normal", 2, (-(2 ** 20), 2 ** 20)),
+        Workload("ring243_B_32MiB", (243,), "B", 8_388_608, "normal", 2, (-(2 ** 20), 2 ** 20),
+                 True),
         Workload("torus27x27_B_4MiB", (27, 27), "B", 1_048_576, "normal", 3, None, True),
-        Workload("torus9x9x9_B_128MiB", (9, 9, 9), "B", 33_554_432, "hash_uniform", 4, None),
+        Workload("torus9x9x9_B_128MiB", (9, 9, 9), "B", 33_554_432, "hash_uniform", 4, None,
+                 True),
         # rings whose size is not a power of three (the paper's 8- and 64-node rings)
         Workload("ring8_B_32MiB", (8,), "B", 8_388_608, "normal", 5, (-(2 ** 20), 2 ** 20), True,
                  ("nonpower3",)),
