@@ -391,3 +391,31 @@ def test_latency_slot_plan_needs_its_workspace():
     assert lib.trivance_workspace_bytes(None, 10, 0) == -1
     assert lib.trivance_workspace_bytes(p.handle, -1, 0) == -1
     assert lib.trivance_workspace_bytes(p.handle, 10, 7) == -1
+
+
+def test_missing_library_fails_loudly():
+    """Every call of the binding reaches the native library through one loader, and every use
+    starts with a plan: without the library, the loader and plan construction raise RuntimeError
+    (there is no fallback path). Checked in a child process whose binding points at a library
+    that does not exist."""
+    import subprocess
+    import sys
+
+    code = (
+        "import paper_2602_17254_amd as T\n"
+        "T.binding.LIB_PATH = '/nonexistent/libtrivance.so'\n"
+        "T.binding._LIB = None\n"
+        "for call in (lambda: T.trivance_plan((9,), 'L'), lambda: T.trivance_plan((3, 3), 'B'),\n"
+        "             T.binding._lib):\n"
+        "    try:\n"
+        "        call()\n"
+        "    except RuntimeError as e:\n"
+        "        assert 'not built' in str(e)\n"
+        "    else:\n"
+        "        raise SystemExit('no error')\n"
+        "print('raised')\n")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    res = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=root,
+                         timeout=300)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert res.stdout.strip().endswith("raised")
