@@ -509,11 +509,14 @@ def copy_probe(nbytes: int, reps: int = 3) -> None:
 
 
 SWEEP_CLASSES = [((81,), "L"), ((243,), "B"), ((27, 27), "B"), ((9, 9, 9), "B"), ((8,), "B"),
-                 ((64,), "B"), ((32, 32), "B"), ((8, 64), "B"), ((16, 16, 16), "B")]
+                 ((64,), "B"), ((32, 32), "B"), ((8, 64), "B"), ((16, 16, 16), "B"),
+                 ((8,), "L"), ((64,), "L"), ((32, 32), "L")]
 # the power-of-three bandwidth-optimal classes again with message-contiguous block placement
 SWEEP_PLACED = [(243,), (27, 27), (9, 9, 9)]
 SWEEP_MIB = [8, 16, 32, 64, 128]
-SWEEP_MAX_RESIDENT = 150 * 2 ** 30  # 16x16x16 stops at 32 MiB per rank (128 GiB resident)
+# buffers plus workspace: 16x16x16 stops at 32 MiB per rank (128 GiB), the latency-optimal 32x32
+# at 8 MiB (8 GiB of buffers and 144 GiB of partial sums)
+SWEEP_MAX_RESIDENT = 160 * 2 ** 30
 
 
 def sweep(steps: int, warmup: int) -> None:
@@ -531,7 +534,7 @@ def sweep(steps: int, warmup: int) -> None:
         n = plan.n
         for mib in SWEEP_MIB:
             E = mib * 2 ** 20 // 4
-            if n * E * 4 > SWEEP_MAX_RESIDENT:
+            if n * E * 4 + T.trivance_workspace_bytes(plan, E) > SWEEP_MAX_RESIDENT:
                 continue
             _say(f"[sweep] {'x'.join(map(str, dims))} {variant} {placement} {mib} MiB per rank")
             buf = torch.empty((n, E), dtype=torch.float32, device="cuda")
@@ -552,7 +555,9 @@ def sweep(steps: int, warmup: int) -> None:
                               "block_placement": placement, "rank_mib": mib, "n_ranks": n, "passes": plan.num_passes,
                               "ms_per_allreduce": round(ms, 4), "GBps": round(gbps, 1),
                               "pct_of_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
-                              "resident_GB": round(n * E * 4 / 1e9, 2)}), flush=True)
+                              "resident_GB": round(n * E * 4 / 1e9, 2),
+                              "workspace_GB": round(T.trivance_workspace_bytes(plan, E) / 1e9, 2)}),
+                  flush=True)
             del buf, ws
             torch.cuda.empty_cache()
 
