@@ -35,8 +35,6 @@ so some messages carry more than one vector (the cost model counts them).
 
 from __future__ import annotations
 
-from itertools import product
-
 import numpy as np
 
 from . import nonpow3

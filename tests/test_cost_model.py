@@ -11,7 +11,6 @@ import math
 import sys
 from fractions import Fraction
 
-import numpy as np
 import pytest
 
 from oracle import cost
