@@ -1,14 +1,17 @@
 """Benchmark of the emulated Trivance AllReduce on one MI355X.
 
-python bench.py [--steps K] [--warmup W] [--workload NAME | --all] [--no-cpu-baseline]
+python bench.py [--steps K] [--warmup W] [--workload NAME | --all] [--dtype f32|i32]
+                [--no-cpu-baseline] [--no-summary]
+python bench.py --sweep [--steps K] [--warmup W]     8..128 MiB per rank for every class
+python bench.py --copy-probe BYTES                   a plain device copy (counter calibration)
 
 A step is one whole emulated AllReduce (every pass of the schedule) over the workload's n rank
 vectors, which are resident in HBM before timing starts. K steps are timed, bracketed by device
 synchronisation; before each, the inputs are restored on the device (outside the events), so
 every timed AllReduce works on the workload's own finite inputs. HIP events on the launch stream
-bracket each step and, inside it, each phase (all passes of the latency-optimal variant; the reduce-scatter and the all-gather), whose
-passes run back to back with one kernel family: group time / launches is that family's average
-launch duration, used for the roofline. One more step after the timed region brackets every pass
+bracket each step and, inside it, each phase (all passes of the latency-optimal variant; the
+reduce-scatter and the all-gather), whose passes run back to back with one kernel family: group
+time / launches is that family's average launch duration, used for the roofline. One more step after the timed region brackets every pass
 with events (per-pass diagnostic only). Throughput counts the algorithmic
 bytes of the step-by-step schedule (each participating location read once and each output
 written once per pass; trivance_algorithmic_bytes).
