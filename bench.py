@@ -412,11 +412,13 @@ SUMMARY_JOBS = [("ring9_L_4KiB", "f32"), ("ring81_L_8MiB", "f32"), ("ring243_B_3
                 ("ring243_B_32MiB", "i32"), ("torus27x27_B_4MiB", "f32")]
 
 
-def summary_line(w, dtype, steps=10, warmup=2):
+def summary_line(w, dtype, steps=10, warmup=2, with_cpu=True):
     """Throughput of one more configuration in the same run, with inputs from torch's seeded
     device generator (the workload's distribution) restored before every timed AllReduce, and a
     check of the result on the device: int32 against the exact column sums, fp32 within
-    4 ceil(log3 n) 2^-23 sum|v| of an fp64 sum."""
+    4 ceil(log3 n) 2^-23 sum|v| of an fp64 sum. With with_cpu, the oracle is also timed on one
+    core on a column sample of the same inputs (about 3 s) and compared with the GPU result on
+    those columns (`cpu_baseline`)."""
     import torch
 
     import paper_2602_17254_amd as T
@@ -453,6 +455,15 @@ def summary_line(w, dtype, steps=10, warmup=2):
             bound = 4.0 * steps_bound * 2.0 ** -23 * x.abs().sum(0)
             err = (out[:, e0:e1].to(torch.float64) - x.sum(0)[None, :]).abs()
             ok = ok and bool((err <= bound[None, :]).all())
+    oracle = None
+    if with_cpu:
+        budget = {"L": 1 << 18, "B": min(12_000, (1 << 22) // w.n)}[w.variant]
+        cols = _sample_for_baseline(w, min(budget, w.elems))
+        idx = torch.from_numpy(cols).cuda()
+        V_cols = buf.index_select(1, idx).cpu().numpy()
+        got_cols = out.index_select(1, idx).cpu().numpy()
+        oracle = cpu_baseline(w, got_cols, cols, V_cols, seconds_target=3.0, max_runs=10)
+        oracle.pop("host", None)
     del buf, regen, out
     torch.cuda.empty_cache()
     gbps = alg_bytes / (ms * 1e-3) / 1e9
@@ -462,7 +473,7 @@ def summary_line(w, dtype, steps=10, warmup=2):
             ("N(0,1)" if dtype == "f32" else f"uniform int32 {w.int_range}"),
             "result_check": ("exact column sums" if dtype == "i32" else
                              "within 4 ceil(log3 n) 2^-23 sum|v| of fp64"),
-            "result_ok": ok}
+            "result_ok": ok, **({"cpu_baseline": oracle} if oracle else {})}
 
 
 def copy_ceiling(nbytes: int = 1 << 30, reps: int = 10) -> dict:
@@ -602,7 +613,9 @@ def main():
         line = run_workload(inputs.WORKLOADS[name], args.steps, args.warmup,
                             with_cpu=not args.no_cpu_baseline, dtype=dtype)
         if not args.all and not args.no_summary and name == inputs.HEADLINE:
-            line["other_configs"] = [summary_line(inputs.WORKLOADS[n], d) for n, d in SUMMARY_JOBS]
+            line["other_configs"] = [summary_line(inputs.WORKLOADS[n], d,
+                                                  with_cpu=not args.no_cpu_baseline)
+                                     for n, d in SUMMARY_JOBS]
         print(json.dumps(line), flush=True)
 
 
