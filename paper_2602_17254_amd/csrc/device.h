@@ -74,6 +74,38 @@ __device__ __forceinline__ void st(T* p, const Vec<T, N>& v) {
     }
 }
 
+// Streaming store through a raw buffer descriptor with the instruction cache-policy bits NT and
+// SC1 set: the write-once outputs of the block steps measured 1-3.5% faster this way than with NT
+// alone (global_store ... nt), on the 243-ring, 27x27 and 9x9x9 in both phases. `base` is
+// wave-uniform and `bytes` the bytes from it that are valid: a lane whose byte offset lies beyond
+// writes nothing (the descriptor's range check), so a ragged tail needs no predicate.
+typedef int BufI4 __attribute__((ext_vector_type(4)));
+__device__ void raw_buffer_store_v4i32(BufI4 data, BufI4 rsrc, int voffset, int soffset,
+                                       int cpol) __asm("llvm.amdgcn.raw.buffer.store.v4i32");
+__device__ void raw_buffer_store_i32(int data, BufI4 rsrc, int voffset, int soffset,
+                                     int cpol) __asm("llvm.amdgcn.raw.buffer.store.i32");
+constexpr int kCpolStream = 2 | 16;  // NT | SC1
+
+__device__ __forceinline__ BufI4 buffer_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    BufI4 r;
+    r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    r.y = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xFFFFu));  // stride 0
+    r.z = __builtin_amdgcn_readfirstlane((int)bytes);                           // num_records
+    r.w = 0x00020000;  // raw 32-bit data format (gfx9 family)
+    return r;
+}
+
+template <typename T, int N>
+__device__ __forceinline__ void st_stream(BufI4 rsrc, uint32_t byte_offset, const Vec<T, N>& v) {
+    static_assert(sizeof(T) == 4 && (N == 1 || N == 4), "32-bit elements, 4- or 16-byte stores");
+    if constexpr (N == 4) {
+        raw_buffer_store_v4i32(__builtin_bit_cast(BufI4, v), rsrc, (int)byte_offset, 0, kCpolStream);
+    } else {
+        raw_buffer_store_i32(__builtin_bit_cast(int, v), rsrc, (int)byte_offset, 0, kCpolStream);
+    }
+}
+
 __device__ __forceinline__ int64_t imin64(int64_t a, int64_t b) { return a < b ? a : b; }
 
 // Workgroup index remapped so that each of the 8 XCDs (which receive workgroups round-robin)

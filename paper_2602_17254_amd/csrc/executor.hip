@@ -222,6 +222,13 @@ __global__ __launch_bounds__(64 * P) void latency_split_kernel(T* __restrict__ b
     const int64_t rowstep = (int64_t)dist * stride * E;
     T* const col = buf + (int64_t)first_rank * E + seg_b + (ok ? v_idx : 0) * VEC +
                    (int64_t)(w * SUB) * rowstep;
+    // stores: streaming buffer stores; the wave's 64 columns of row i start at wcol + i rowstep
+    T* const wcol = buf + (int64_t)first_rank * E + seg_b + (int64_t)cb * 64 * VEC +
+                    (int64_t)(w * SUB) * rowstep;
+    const int64_t wvec = nvec - (int64_t)cb * 64;  // column vectors of this block that exist
+    const uint32_t nbytes =
+        wvec > 0 ? (uint32_t)(imin64(wvec, 64) * VEC * (int64_t)sizeof(T)) : 0u;
+    const uint32_t off = (uint32_t)lane * VEC * (uint32_t)sizeof(T);
 
     V v[SUB];
     if (ok) {
@@ -246,7 +253,8 @@ __global__ __launch_bounds__(64 * P) void latency_split_kernel(T* __restrict__ b
         for (int i = 3 * g; i < 3 * g + 3; ++i) {
             const V& left = i == 0 ? before : v[i > 0 ? i - 1 : 0];
             const V& right = i == SUB - 1 ? after : v[i + 1 < SUB ? i + 1 : i];
-            st<T, VEC, NT>(col + (int64_t)i * rowstep, joint(v[i], left, right));
+            st_stream<T, VEC>(buffer_rsrc(wcol + (int64_t)i * rowstep, nbytes), off,
+                              joint(v[i], left, right));
         }
     }
 }
@@ -366,6 +374,8 @@ __global__ __launch_bounds__(64 * WPB) void block_step_kernel(T* __restrict__ bu
         idx[u] = w.begin + (int64_t)(u * 64 + lane) * VEC;
         ok[u] = idx[u] < w.end;
     }
+    // stores: streaming buffer stores over this wave's chunk (the descriptor ends at the block)
+    const uint32_t nbytes = (uint32_t)(imin64(w.end - w.begin, kChunk) * (int64_t)sizeof(T));
     if constexpr (REDUCE) {
         V x[U], y[U], z[U];
 #pragma unroll
@@ -376,19 +386,24 @@ __global__ __launch_bounds__(64 * WPB) void block_step_kernel(T* __restrict__ bu
                 z[u] = ld<T, VEC, NT>(pr + idx[u]);
             }
         }
+        const BufI4 ro = buffer_rsrc(own + w.begin, nbytes);
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (ok[u]) st<T, VEC, NT>(own + idx[u], joint(x[u], y[u], z[u]));
+            if (ok[u])
+                st_stream<T, VEC>(ro, (uint32_t)(u * 64 + lane) * VEC * sizeof(T),
+                                  joint(x[u], y[u], z[u]));
     } else {
         V x[U];
 #pragma unroll
         for (int u = 0; u < U; ++u)
             if (ok[u]) x[u] = ld<T, VEC, NT>(own + idx[u]);
+        const BufI4 rl = buffer_rsrc(pl + w.begin, nbytes), rr = buffer_rsrc(pr + w.begin, nbytes);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (ok[u]) {
-                st<T, VEC, NT>(pl + idx[u], x[u]);
-                st<T, VEC, NT>(pr + idx[u], x[u]);
+                const uint32_t off = (uint32_t)(u * 64 + lane) * VEC * sizeof(T);
+                st_stream<T, VEC>(rl, off, x[u]);
+                st_stream<T, VEC>(rr, off, x[u]);
             }
         }
     }
@@ -600,6 +615,8 @@ __global__ __launch_bounds__(64) void tree_step_kernel(T* __restrict__ buf, Tree
     const uint32_t wg = a.wg_base + xcd_contiguous(blockIdx.x, gridDim.x);
     const uint32_t first = wg * (uint32_t)U;
     int64_t po[U], pl[U], pr[U];
+    int64_t co[U], cl[U], cr[U];  // wave-uniform element offsets of the unit's chunk in the rows
+    uint32_t nb[U];               // bytes of the chunk that belong to the block
     uint32_t fl[U];
     bool ok[U];
     V vo[U], vl[U], vr[U];
@@ -608,8 +625,13 @@ __global__ __launch_bounds__(64) void tree_step_kernel(T* __restrict__ buf, Tree
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         if (u > 0 && live) live = tree_next(a, first + u, &w);
-        const int64_t idx = w.b + (int64_t)w.chunk * kChunk + (int64_t)lane * VEC;
+        const int64_t cs = w.b + (int64_t)w.chunk * kChunk;
+        const int64_t idx = cs + (int64_t)lane * VEC;
         ok[u] = live && idx < w.e;
+        nb[u] = live && cs < w.e ? (uint32_t)(imin64(w.e - cs, kChunk) * (int64_t)sizeof(T)) : 0u;
+        co[u] = w.row + cs;
+        cl[u] = w.rl + cs;
+        cr[u] = w.rr + cs;
         po[u] = w.row + idx;
         pl[u] = w.rl + idx;
         pr[u] = w.rr + idx;
@@ -622,6 +644,8 @@ __global__ __launch_bounds__(64) void tree_step_kernel(T* __restrict__ buf, Tree
             }
         }
     }
+    // stores: streaming buffer stores over each unit's chunk (the descriptor ends at the block)
+    const uint32_t off = (uint32_t)lane * VEC * (uint32_t)sizeof(T);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         if (!ok[u]) continue;
@@ -629,10 +653,10 @@ __global__ __launch_bounds__(64) void tree_step_kernel(T* __restrict__ buf, Tree
             V acc = vo[u];
             if (fl[u] & kFromLeft) acc = vadd(acc, vl[u]);
             if (fl[u] & kFromRight) acc = vadd(acc, vr[u]);
-            st<T, VEC, true>(buf + po[u], acc);
+            st_stream<T, VEC>(buffer_rsrc(buf + co[u], nb[u]), off, acc);
         } else {
-            if (fl[u] & kFromLeft) st<T, VEC, true>(buf + pl[u], vo[u]);
-            if (fl[u] & kFromRight) st<T, VEC, true>(buf + pr[u], vo[u]);
+            if (fl[u] & kFromLeft) st_stream<T, VEC>(buffer_rsrc(buf + cl[u], nb[u]), off, vo[u]);
+            if (fl[u] & kFromRight) st_stream<T, VEC>(buffer_rsrc(buf + cr[u], nb[u]), off, vo[u]);
         }
     }
 }

@@ -100,7 +100,12 @@ __global__ __launch_bounds__(64 * kSlotWaves) void slot_step_kernel(T* __restric
     const T* const own_row = in + (int64_t)x * E + col0;
     const T* const left_row = in + (int64_t)xl * E + col0;
     const T* const right_row = in + (int64_t)xr * E + col0;
-    T* const out_row = out + (int64_t)x * E + col0;
+    // stores: streaming buffer stores over the wave's 64 column vectors of each output partial
+    T* const out_wave = out + (int64_t)x * E + seg_b + (int64_t)cb * kSlotChunks * 64 * VEC;
+    const uint32_t nbytes = (uint32_t)(imin64(seg_e - (seg_b + (int64_t)cb * kSlotChunks * 64 * VEC),
+                                              (int64_t)kSlotChunks * 64 * VEC) *
+                                       (int64_t)sizeof(T));
+    const uint32_t off = (uint32_t)(threadIdx.x & 63) * VEC * (uint32_t)sizeof(T);
     // outputs in batches of kSlotBatch: all loads of a batch are issued before its stores
     for (int k0 = 0; k0 < a.nout[c]; k0 += kSlotBatch) {
         V vo[kSlotBatch][kSlotChunks], vl[kSlotBatch][kSlotChunks], vr[kSlotBatch][kSlotChunks];
@@ -130,8 +135,8 @@ __global__ __launch_bounds__(64 * kSlotWaves) void slot_step_kernel(T* __restric
                 V acc = so[b] >= 0 ? vo[b][u] : (sl[b] >= 0 ? vl[b][u] : vr[b][u]);
                 if (so[b] >= 0 && sl[b] >= 0) acc = vadd(acc, vl[b][u]);
                 if (sr[b] >= 0 && (so[b] >= 0 || sl[b] >= 0)) acc = vadd(acc, vr[b][u]);
-                st<T, VEC, true>(out_row + (int64_t)(k0 + b) * a.slot_stride +
-                                     (int64_t)u * 64 * VEC, acc);
+                st_stream<T, VEC>(buffer_rsrc(out_wave + (int64_t)(k0 + b) * a.slot_stride, nbytes),
+                                  off + (uint32_t)(u * 64 * VEC * sizeof(T)), acc);
             }
         }
     }}
