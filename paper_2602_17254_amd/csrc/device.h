@@ -74,17 +74,26 @@ __device__ __forceinline__ void st(T* p, const Vec<T, N>& v) {
     }
 }
 
-// Streaming store through a raw buffer descriptor with the instruction cache-policy bits NT and
-// SC1 set: the write-once outputs of the block steps measured 1-3.5% faster this way than with NT
-// alone (global_store ... nt), on the 243-ring, 27x27 and 9x9x9 in both phases. `base` is
-// wave-uniform and `bytes` the bytes from it that are valid: a lane whose byte offset lies beyond
-// writes nothing (the descriptor's range check), so a ragged tail needs no predicate.
+// Store of a write-once output through a raw buffer descriptor, with one of two instruction
+// cache policies chosen per pass by the host (`keep`, wave-uniform):
+//  * keep = 0: NT | SC1 (streaming). Passes over gigabytes measured 1-3.5% faster this way than
+//    with NT alone (global_store ... nt) on the 243-ring, the 27x27 and the 9x9x9 tori, both
+//    phases, and 6-17% faster than with the default policy.
+//  * keep = 1: SC1 alone. A pass whose algorithmic bytes stay within kKeepPassBytes writes about
+//    the size of the 256 MB last-level (MALL) cache or less, and the next pass reads what it
+//    wrote: with NT those lines leave the cache; without it the ring of 8 at 32 MiB per rank and
+//    the ring of 64 at 8 MiB (bandwidth-optimal) measured 9% faster, and their small late passes
+//    up to 20%.
+// `base` is wave-uniform and `bytes` the bytes from it that are valid: a lane whose byte offset
+// lies beyond writes nothing (the descriptor's range check), so a ragged tail needs no predicate.
 typedef int BufI4 __attribute__((ext_vector_type(4)));
 __device__ void raw_buffer_store_v4i32(BufI4 data, BufI4 rsrc, int voffset, int soffset,
                                        int cpol) __asm("llvm.amdgcn.raw.buffer.store.v4i32");
 __device__ void raw_buffer_store_i32(int data, BufI4 rsrc, int voffset, int soffset,
                                      int cpol) __asm("llvm.amdgcn.raw.buffer.store.i32");
 constexpr int kCpolStream = 2 | 16;  // NT | SC1
+constexpr int kCpolKeep = 16;        // SC1
+constexpr int64_t kKeepPassBytes = (int64_t)1 << 30;
 
 __device__ __forceinline__ BufI4 buffer_rsrc(const void* base, uint32_t bytes) {
     const uint64_t a = reinterpret_cast<uint64_t>(base);
@@ -96,14 +105,23 @@ __device__ __forceinline__ BufI4 buffer_rsrc(const void* base, uint32_t bytes) {
     return r;
 }
 
-template <typename T, int N>
-__device__ __forceinline__ void st_stream(BufI4 rsrc, uint32_t byte_offset, const Vec<T, N>& v) {
+template <int KEEP, typename T, int N>
+__device__ __forceinline__ void st_out_as(BufI4 rsrc, uint32_t byte_offset, const Vec<T, N>& v) {
     static_assert(sizeof(T) == 4 && (N == 1 || N == 4), "32-bit elements, 4- or 16-byte stores");
+    constexpr int cpol = KEEP ? kCpolKeep : kCpolStream;
     if constexpr (N == 4) {
-        raw_buffer_store_v4i32(__builtin_bit_cast(BufI4, v), rsrc, (int)byte_offset, 0, kCpolStream);
+        raw_buffer_store_v4i32(__builtin_bit_cast(BufI4, v), rsrc, (int)byte_offset, 0, cpol);
     } else {
-        raw_buffer_store_i32(__builtin_bit_cast(int, v), rsrc, (int)byte_offset, 0, kCpolStream);
+        raw_buffer_store_i32(__builtin_bit_cast(int, v), rsrc, (int)byte_offset, 0, cpol);
     }
+}
+
+// The policy as a wave-uniform run-time flag: one scalar branch per store.
+template <typename T, int N>
+__device__ __forceinline__ void st_out(BufI4 rsrc, uint32_t byte_offset, const Vec<T, N>& v,
+                                       int keep) {
+    if (keep) st_out_as<1>(rsrc, byte_offset, v);
+    else st_out_as<0>(rsrc, byte_offset, v);
 }
 
 __device__ __forceinline__ int64_t imin64(int64_t a, int64_t b) { return a < b ? a : b; }

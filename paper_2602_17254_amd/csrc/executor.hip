@@ -88,6 +88,7 @@ struct StepArgs {
     FastDiv f_mod[kMaxDims][kMaxDims];   // modulus[c][d]
     FastDiv f_nq[kMaxDims][kMaxDims];    // dims[d] / modulus[c][d]
     uint32_t wg_base;              // first workgroup of this dispatch (for_each_dispatch)
+    int keep;                      // store policy of the pass (st_out)
     // block steps of plans placed by schedule digits (TRIVANCE_PLACE_BY_SCHEDULE)
     // (32-bit words: the scalar unit loads them directly; bytes would go through vector loads)
     int placed;
@@ -190,7 +191,7 @@ __global__ __launch_bounds__(kBlockThreads) void latency_step_kernel(T* __restri
 // wave publishes its own first and last row in LDS and reads its neighbours' after one barrier,
 // before any store, so the in-place update stays correct. Splitting gives P times more, P times
 // shorter wavefronts than walking the whole cycle in one wavefront.
-template <typename T, int VEC, int SUB, int P, int PD, bool NT>
+template <typename T, int VEC, int SUB, int P, int PD, bool NT, int KEEP>
 __global__ __launch_bounds__(64 * P) void latency_split_kernel(T* __restrict__ buf, StepArgs a) {
     static_assert(SUB % 3 == 0, "rows are processed in groups of three");
     using V = Vec<T, VEC>;
@@ -253,8 +254,8 @@ __global__ __launch_bounds__(64 * P) void latency_split_kernel(T* __restrict__ b
         for (int i = 3 * g; i < 3 * g + 3; ++i) {
             const V& left = i == 0 ? before : v[i > 0 ? i - 1 : 0];
             const V& right = i == SUB - 1 ? after : v[i + 1 < SUB ? i + 1 : i];
-            st_stream<T, VEC>(buffer_rsrc(wcol + (int64_t)i * rowstep, nbytes), off,
-                              joint(v[i], left, right));
+            st_out_as<KEEP>(buffer_rsrc(wcol + (int64_t)i * rowstep, nbytes), off,
+                            joint(v[i], left, right));
         }
     }
 }
@@ -390,8 +391,8 @@ __global__ __launch_bounds__(64 * WPB) void block_step_kernel(T* __restrict__ bu
 #pragma unroll
         for (int u = 0; u < U; ++u)
             if (ok[u])
-                st_stream<T, VEC>(ro, (uint32_t)(u * 64 + lane) * VEC * sizeof(T),
-                                  joint(x[u], y[u], z[u]));
+                st_out<T, VEC>(ro, (uint32_t)(u * 64 + lane) * VEC * sizeof(T),
+                               joint(x[u], y[u], z[u]), a.keep);
     } else {
         V x[U];
 #pragma unroll
@@ -402,8 +403,8 @@ __global__ __launch_bounds__(64 * WPB) void block_step_kernel(T* __restrict__ bu
         for (int u = 0; u < U; ++u) {
             if (ok[u]) {
                 const uint32_t off = (uint32_t)(u * 64 + lane) * VEC * sizeof(T);
-                st_stream<T, VEC>(rl, off, x[u]);
-                st_stream<T, VEC>(rr, off, x[u]);
+                st_out<T, VEC>(rl, off, x[u], a.keep);
+                st_out<T, VEC>(rr, off, x[u], a.keep);
             }
         }
     }
@@ -466,6 +467,7 @@ struct TreeArgs {
     FastDiv32 f_side[DM];
     TreeColl<DM> coll[DM];
     uint32_t wg_base;     // first workgroup of this dispatch (for_each_dispatch)
+    int keep;             // store policy of the pass (st_out)
     uint32_t tab[CAP];
 };
 static_assert(sizeof(TreeArgs<kMaxTreeDims, kMaxTab>) <= 4096,
@@ -653,10 +655,12 @@ __global__ __launch_bounds__(64) void tree_step_kernel(T* __restrict__ buf, Tree
             V acc = vo[u];
             if (fl[u] & kFromLeft) acc = vadd(acc, vl[u]);
             if (fl[u] & kFromRight) acc = vadd(acc, vr[u]);
-            st_stream<T, VEC>(buffer_rsrc(buf + co[u], nb[u]), off, acc);
+            st_out<T, VEC>(buffer_rsrc(buf + co[u], nb[u]), off, acc, a.keep);
         } else {
-            if (fl[u] & kFromLeft) st_stream<T, VEC>(buffer_rsrc(buf + cl[u], nb[u]), off, vo[u]);
-            if (fl[u] & kFromRight) st_stream<T, VEC>(buffer_rsrc(buf + cr[u], nb[u]), off, vo[u]);
+            if (fl[u] & kFromLeft)
+                st_out<T, VEC>(buffer_rsrc(buf + cl[u], nb[u]), off, vo[u], a.keep);
+            if (fl[u] & kFromRight)
+                st_out<T, VEC>(buffer_rsrc(buf + cr[u], nb[u]), off, vo[u], a.keep);
         }
     }
 }
@@ -809,7 +813,13 @@ hipError_t launch_split(T* buf, StepArgs a, Launch L, const Exec& x) {
     constexpr size_t halo = (size_t)P * 2 * 64 * sizeof(Vec<T, VEC>);  // the kernel's own LDS
     constexpr size_t extra = cap ? kLdsPerCu / cap - halo - kLdsSlack : 0;  // unused: the cap
     static_assert(extra + halo <= kLdsPerCu, "a workgroup must fit in one CU's LDS");
-    return dispatch(latency_split_kernel<T, VEC, SUB, P, 1, true>, L.grid, 64 * P, x, buf, a,
+    // the store policy (st_out_as) as a template argument: a branch per store measured 6% slower
+    // on the 9x9x9 torus at 8 MiB per rank, and one branch around the walk doubled the registers
+    // of the 81-row walks
+    if (a.keep)
+        return dispatch(latency_split_kernel<T, VEC, SUB, P, 1, true, 1>, L.grid, 64 * P, x, buf,
+                        a, extra);
+    return dispatch(latency_split_kernel<T, VEC, SUB, P, 1, true, 0>, L.grid, 64 * P, x, buf, a,
                     extra);
 }
 
@@ -867,6 +877,7 @@ int run_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t 
         Launch L;
         rc = pass_args<VEC>(p, ps, max_blk, 1, &a, &L);
         if (rc != TRIVANCE_OK) return rc;
+        a.keep = trivance_pass_bytes(p, elems, TRIVANCE_F32, pi) <= kKeepPassBytes;
         hipError_t err = hipSuccess;
         if (ps.phase == TRIVANCE_PHASE_LATENCY) {
             // collectives that share a cycle length run in one launch; with equal sides that is
@@ -976,6 +987,7 @@ int run_tree_impl(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t s
         }
         a.total = (uint32_t)total;
         if (total == 0) continue;
+        a.keep = trivance_pass_bytes(p, elems, TRIVANCE_F32, pi) <= kKeepPassBytes;
         const bool rs = ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER;
         hipError_t err;
         switch (rs ? u_rs : u_ag) {

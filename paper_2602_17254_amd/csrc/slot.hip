@@ -47,6 +47,7 @@ struct SlotArgs {
     FastDiv32 f_cycle[kMaxDims], f_gcyc[kMaxDims], f_side[kMaxDims], f_stride[kMaxDims];
     int8_t own[kMaxDims][kMaxSlots], left[kMaxDims][kMaxSlots], right[kMaxDims][kMaxSlots];
     uint32_t wg_base;
+    int keep;  // store policy of the pass (st_out)
 };
 static_assert(sizeof(SlotArgs) <= 4096, "slot-step kernel arguments above 4 KiB");
 
@@ -135,8 +136,8 @@ __global__ __launch_bounds__(64 * kSlotWaves) void slot_step_kernel(T* __restric
                 V acc = so[b] >= 0 ? vo[b][u] : (sl[b] >= 0 ? vl[b][u] : vr[b][u]);
                 if (so[b] >= 0 && sl[b] >= 0) acc = vadd(acc, vl[b][u]);
                 if (sr[b] >= 0 && (so[b] >= 0 || sl[b] >= 0)) acc = vadd(acc, vr[b][u]);
-                st_stream<T, VEC>(buffer_rsrc(out_wave + (int64_t)(k0 + b) * a.slot_stride, nbytes),
-                                  off + (uint32_t)(u * 64 * VEC * sizeof(T)), acc);
+                st_out<T, VEC>(buffer_rsrc(out_wave + (int64_t)(k0 + b) * a.slot_stride, nbytes),
+                               off + (uint32_t)(u * 64 * VEC * sizeof(T)), acc, a.keep);
             }
         }
     }}
@@ -180,6 +181,7 @@ int run_slot_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, T* ws, 
     for (int pi = pb; pi < pe; ++pi) {
         const Pass& ps = p->passes[pi];
         const SlotPass& sp = p->slots[pi];
+        a.keep = trivance_pass_bytes(p, elems, TRIVANCE_F32, pi) <= kKeepPassBytes;
         for (int c = 0; c < p->D; ++c) {
             a.act[c] = ps.dim[c];
             a.dist[c] = ps.distance[c];
