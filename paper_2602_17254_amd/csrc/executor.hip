@@ -101,8 +101,9 @@ struct StepArgs {
 
 // ---------------------------------------------------------------------------------------------
 // Latency-optimal step: sliding window over one rank cycle.
-// Grid: D * ncycles * colblocks thread blocks; each thread owns VPT column vectors.
-template <typename T, int VEC, int VPT>
+// Grid: D * ncycles * colblocks thread blocks; each thread owns VPT column vectors. Non-temporal
+// loads; stores with the pass's policy (st_out_as), a template argument as in the tiles below.
+template <typename T, int VEC, int VPT, int KEEP>
 __global__ __launch_bounds__(kBlockThreads) void latency_step_kernel(T* __restrict__ buf,
                                                                      StepArgs a) {
     using V = Vec<T, VEC>;
@@ -130,21 +131,29 @@ __global__ __launch_bounds__(kBlockThreads) void latency_step_kernel(T* __restri
 
     T* col[VPT];
     bool ok[VPT];
+    // stores: the wave's 64 column vectors of row i start at wcol[u] + i rowstep
+    const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t off = (threadIdx.x & 63) * VEC * (uint32_t)sizeof(T);
+    T* wcol[VPT];
+    uint32_t nb[VPT];
 #pragma unroll
     for (int u = 0; u < VPT; ++u) {
         const int64_t v = ((int64_t)cb * VPT + u) * kBlockThreads + threadIdx.x;
         ok[u] = v < nvec;
         col[u] = base + v * VEC;
+        const int64_t w = ((int64_t)cb * VPT + u) * kBlockThreads + (int64_t)wave * 64;
+        wcol[u] = base + w * VEC;
+        nb[u] = nvec > w ? (uint32_t)(imin64(nvec - w, 64) * VEC * (int64_t)sizeof(T)) : 0u;
     }
 
     V first[VPT], last[VPT], prev[VPT], a0[VPT], a1[VPT], a2[VPT];
 #pragma unroll
     for (int u = 0; u < VPT; ++u) {
         if (ok[u]) {
-            last[u] = ld<T, VEC>(col[u] + (int64_t)(len - 1) * rowstep);
-            first[u] = ld<T, VEC>(col[u]);
-            a1[u] = ld<T, VEC>(col[u] + rowstep);
-            a2[u] = len == 3 ? last[u] : ld<T, VEC>(col[u] + 2 * rowstep);
+            last[u] = ld<T, VEC, true>(col[u] + (int64_t)(len - 1) * rowstep);
+            first[u] = ld<T, VEC, true>(col[u]);
+            a1[u] = ld<T, VEC, true>(col[u] + rowstep);
+            a2[u] = len == 3 ? last[u] : ld<T, VEC, true>(col[u] + 2 * rowstep);
             prev[u] = last[u];
             a0[u] = first[u];
         }
@@ -157,10 +166,11 @@ __global__ __launch_bounds__(kBlockThreads) void latency_step_kernel(T* __restri
         for (int u = 0; u < VPT; ++u) {
             if (ok[u]) {
                 if (more) {
-                    b0[u] = ld<T, VEC>(col[u] + (int64_t)(i + 3) * rowstep);
-                    b1[u] = ld<T, VEC>(col[u] + (int64_t)(i + 4) * rowstep);
-                    b2[u] = (i + 5 == len - 1) ? last[u]
-                                               : ld<T, VEC>(col[u] + (int64_t)(i + 5) * rowstep);
+                    b0[u] = ld<T, VEC, true>(col[u] + (int64_t)(i + 3) * rowstep);
+                    b1[u] = ld<T, VEC, true>(col[u] + (int64_t)(i + 4) * rowstep);
+                    b2[u] = (i + 5 == len - 1)
+                                ? last[u]
+                                : ld<T, VEC, true>(col[u] + (int64_t)(i + 5) * rowstep);
                 } else {
                     b0[u] = first[u];
                     b1[u] = first[u];
@@ -171,10 +181,11 @@ __global__ __launch_bounds__(kBlockThreads) void latency_step_kernel(T* __restri
 #pragma unroll
         for (int u = 0; u < VPT; ++u) {
             if (ok[u]) {
-                T* p = col[u] + (int64_t)i * rowstep;
-                st<T, VEC>(p, joint(a0[u], prev[u], a1[u]));
-                st<T, VEC>(p + rowstep, joint(a1[u], a0[u], a2[u]));
-                st<T, VEC>(p + 2 * rowstep, joint(a2[u], a1[u], b0[u]));
+                T* p = wcol[u] + (int64_t)i * rowstep;
+                st_out_as<KEEP>(buffer_rsrc(p, nb[u]), off, joint(a0[u], prev[u], a1[u]));
+                st_out_as<KEEP>(buffer_rsrc(p + rowstep, nb[u]), off, joint(a1[u], a0[u], a2[u]));
+                st_out_as<KEEP>(buffer_rsrc(p + 2 * rowstep, nb[u]), off,
+                                joint(a2[u], a1[u], b0[u]));
                 prev[u] = a2[u];
                 a0[u] = b0[u];
                 a1[u] = b1[u];
@@ -842,7 +853,10 @@ hipError_t launch_latency(T* buf, const StepArgs& a, const Launch& L, int len, c
             StepArgs b = a;
             Launch M = L;
             set_columns(&b, &M, kBlockThreads);
-            return dispatch(latency_step_kernel<T, VEC, 1>, M.grid, kBlockThreads, x, buf, b);
+            if (b.keep)
+                return dispatch(latency_step_kernel<T, VEC, 1, 1>, M.grid, kBlockThreads, x, buf,
+                                b);
+            return dispatch(latency_step_kernel<T, VEC, 1, 0>, M.grid, kBlockThreads, x, buf, b);
         }
     }
 }
