@@ -2,10 +2,10 @@
 of 1 to 30 (powers of three or not, equal or not), both variants, fp32 and int32, against the
 oracle element by element (fp32 identical bits, int32 exact).
 
-The sample is drawn once from a fixed seed, so every case has a stable name; it complements the
-hand-picked shapes of the other parity tests with combinations nobody chose: unequal sides mixing
-trees and powers of three, sides of 1 inside tori, element counts with ragged tails, the scalar
-path (E % 4 != 0) and empty segments (E < 64 D). Shapes a plan rejects by design (more partial
+The sample (128 shapes) is drawn once from a fixed seed, so every case has a stable name; it
+complements the hand-picked shapes of the other parity tests with combinations nobody chose:
+unequal sides mixing trees and powers of three, sides of 1 inside tori, element counts with ragged
+tails, the scalar path (E % 4 != 0) and empty segments (E < 64 D). Shapes a plan rejects by design (more partial
 sums than a latency-optimal plan keeps) are skipped with the reason.
 """
 
@@ -35,7 +35,7 @@ def _gpu_present():
     yield
 
 
-def _sample(count=48, seed=20260217, max_ranks=240):
+def _sample(count=128, seed=20260217, max_ranks=240):
     rng = np.random.default_rng(seed)
     out = []
     while len(out) < count:
