@@ -82,10 +82,8 @@ __device__ __forceinline__ void st(T* p, const Vec<T, N>& v) {
 //  * keep = 1: SC1 alone. A pass whose algorithmic bytes stay within kKeepPassBytes writes about
 //    the size of the 256 MB last-level (MALL) cache or less, and the next pass reads what it
 //    wrote: with NT those lines leave the cache; without it the ring of 8 at 32 MiB per rank and
-//    the ring of 64 at 8 MiB (bandwidth-optimal) measured 9% faster, and their small late passes
-//    up to 20%.
-// `base` is wave-uniform and `bytes` the bytes from it that are valid: a lane whose byte offset
-// lies beyond writes nothing (the descriptor's range check), so a ragged tail needs no predicate.
+//    the ring of 64 at 8 MiB (bandwidth-optimal) measured 9-10% faster, and their small late
+//    passes up to 20%.
 typedef int BufI4 __attribute__((ext_vector_type(4)));
 __device__ void raw_buffer_store_v4i32(BufI4 data, BufI4 rsrc, int voffset, int soffset,
                                        int cpol) __asm("llvm.amdgcn.raw.buffer.store.v4i32");
@@ -95,6 +93,15 @@ constexpr int kCpolStream = 2 | 16;  // NT | SC1
 constexpr int kCpolKeep = 16;        // SC1
 constexpr int64_t kKeepPassBytes = (int64_t)1 << 30;
 
+// The store policy of pass `pass` of plan p over rows of `elems` elements (1: SC1 alone). Both
+// element types are 4 bytes wide, so the pass's bytes do not depend on which one a call moves.
+inline int keep_stores(const trivance_plan_t* p, int64_t elems, int pass) {
+    return trivance_pass_bytes(p, elems, TRIVANCE_F32, pass) <= kKeepPassBytes ? 1 : 0;
+}
+
+// Raw buffer descriptor of the `bytes` bytes from the wave-uniform `base`: a lane whose byte
+// offset lies beyond writes nothing (the descriptor's range check), so a ragged tail needs no
+// predicate.
 __device__ __forceinline__ BufI4 buffer_rsrc(const void* base, uint32_t bytes) {
     const uint64_t a = reinterpret_cast<uint64_t>(base);
     BufI4 r;
@@ -105,6 +112,8 @@ __device__ __forceinline__ BufI4 buffer_rsrc(const void* base, uint32_t bytes) {
     return r;
 }
 
+// The value goes to the intrinsic as one reinterpreted vector: assembled component by component,
+// the operand was compiled into one dword repeated four times by this toolchain.
 template <int KEEP, typename T, int N>
 __device__ __forceinline__ void st_out_as(BufI4 rsrc, uint32_t byte_offset, const Vec<T, N>& v) {
     static_assert(sizeof(T) == 4 && (N == 1 || N == 4), "32-bit elements, 4- or 16-byte stores");

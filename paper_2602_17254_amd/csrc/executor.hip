@@ -234,7 +234,8 @@ __global__ __launch_bounds__(64 * P) void latency_split_kernel(T* __restrict__ b
     const int64_t rowstep = (int64_t)dist * stride * E;
     T* const col = buf + (int64_t)first_rank * E + seg_b + (ok ? v_idx : 0) * VEC +
                    (int64_t)(w * SUB) * rowstep;
-    // stores: streaming buffer stores; the wave's 64 columns of row i start at wcol + i rowstep
+    // stores: st_out_as with the pass's policy; the wave's 64 columns of row i start at wcol +
+    // i rowstep
     T* const wcol = buf + (int64_t)first_rank * E + seg_b + (int64_t)cb * 64 * VEC +
                     (int64_t)(w * SUB) * rowstep;
     const int64_t wvec = nvec - (int64_t)cb * 64;  // column vectors of this block that exist
@@ -386,7 +387,7 @@ __global__ __launch_bounds__(64 * WPB) void block_step_kernel(T* __restrict__ bu
         idx[u] = w.begin + (int64_t)(u * 64 + lane) * VEC;
         ok[u] = idx[u] < w.end;
     }
-    // stores: streaming buffer stores over this wave's chunk (the descriptor ends at the block)
+    // stores: buffer stores (st_out) over this wave's chunk (the descriptor ends at the block)
     const uint32_t nbytes = (uint32_t)(imin64(w.end - w.begin, kChunk) * (int64_t)sizeof(T));
     if constexpr (REDUCE) {
         V x[U], y[U], z[U];
@@ -657,7 +658,7 @@ __global__ __launch_bounds__(64) void tree_step_kernel(T* __restrict__ buf, Tree
             }
         }
     }
-    // stores: streaming buffer stores over each unit's chunk (the descriptor ends at the block)
+    // stores: buffer stores (st_out) over each unit's chunk (the descriptor ends at the block)
     const uint32_t off = (uint32_t)lane * VEC * (uint32_t)sizeof(T);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -891,7 +892,7 @@ int run_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t 
         Launch L;
         rc = pass_args<VEC>(p, ps, max_blk, 1, &a, &L);
         if (rc != TRIVANCE_OK) return rc;
-        a.keep = trivance_pass_bytes(p, elems, TRIVANCE_F32, pi) <= kKeepPassBytes;
+        a.keep = keep_stores(p, elems, pi);
         hipError_t err = hipSuccess;
         if (ps.phase == TRIVANCE_PHASE_LATENCY) {
             // collectives that share a cycle length run in one launch; with equal sides that is
@@ -1001,7 +1002,7 @@ int run_tree_impl(T* buf, int64_t elems, const trivance_plan_t* p, hipStream_t s
         }
         a.total = (uint32_t)total;
         if (total == 0) continue;
-        a.keep = trivance_pass_bytes(p, elems, TRIVANCE_F32, pi) <= kKeepPassBytes;
+        a.keep = keep_stores(p, elems, pi);
         const bool rs = ps.phase == TRIVANCE_PHASE_REDUCE_SCATTER;
         hipError_t err;
         switch (rs ? u_rs : u_ag) {

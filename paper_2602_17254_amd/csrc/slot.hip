@@ -101,7 +101,7 @@ __global__ __launch_bounds__(64 * kSlotWaves) void slot_step_kernel(T* __restric
     const T* const own_row = in + (int64_t)x * E + col0;
     const T* const left_row = in + (int64_t)xl * E + col0;
     const T* const right_row = in + (int64_t)xr * E + col0;
-    // stores: streaming buffer stores over the wave's 64 column vectors of each output partial
+    // stores: buffer stores (st_out) over the wave's 64 column vectors of each output partial
     T* const out_wave = out + (int64_t)x * E + seg_b + (int64_t)cb * kSlotChunks * 64 * VEC;
     const uint32_t nbytes = (uint32_t)(imin64(seg_e - (seg_b + (int64_t)cb * kSlotChunks * 64 * VEC),
                                               (int64_t)kSlotChunks * 64 * VEC) *
@@ -181,7 +181,7 @@ int run_slot_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, T* ws, 
     for (int pi = pb; pi < pe; ++pi) {
         const Pass& ps = p->passes[pi];
         const SlotPass& sp = p->slots[pi];
-        a.keep = trivance_pass_bytes(p, elems, TRIVANCE_F32, pi) <= kKeepPassBytes;
+        a.keep = keep_stores(p, elems, pi);
         for (int c = 0; c < p->D; ++c) {
             a.act[c] = ps.dim[c];
             a.dist[c] = ps.distance[c];
