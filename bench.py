@@ -47,13 +47,13 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # summaries are profiles/<kernel>_<workload>.md.
 MEASURED_TRAFFIC = {
     ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {
-        "src": "executor.hip", "src_sha": "30d88ad29958a7c0", "bytes_per_launch": 32568956460},
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 32569005959},
     ("torus9x9x9_B_128MiB", "block_step_kernel<copy>"): {
-        "src": "executor.hip", "src_sha": "30d88ad29958a7c0", "bytes_per_launch": 24427280509},
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 24427297009},
     ("ring64_L_8MiB", "slot_step_kernel"): {
-        "src": "slot.hip", "src_sha": "89d769cc252b392c", "bytes_per_launch": 3233052390},
+        "src": "slot.hip", "src_sha": "3d77914cd8c3b7e8", "bytes_per_launch": 3233236820},
     ("torus32x32_L_8MiB", "slot_step_kernel"): {
-        "src": "slot.hip", "src_sha": "89d769cc252b392c", "bytes_per_launch": 94303931959},
+        "src": "slot.hip", "src_sha": "3d77914cd8c3b7e8", "bytes_per_launch": 94305433906},
 }
 
 
