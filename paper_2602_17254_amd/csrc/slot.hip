@@ -55,8 +55,15 @@ constexpr int kSlotWaves = 4;   // waves per workgroup
 constexpr int kSlotChunks = 1;  // 64-vector chunks of one partial per wave
 constexpr int kSlotGroup = 64;  // consecutive column blocks of one rank in consecutive units
 constexpr int kSlotBatch = 4;   // output partials whose loads are issued together
+// Passes whose bytes fit in the 256 MB last-level cache (MALL) and that write at most two partials
+// per collective take batches of two: 40 instead of 63 VGPRs, so 12 waves per SIMD instead of 8.
+// On the rings of 2, 4 and 8 at 96-288 MiB per pass that measured 4-11% faster per pass, but
+// larger passes with two outputs measured 4-16% slower with it (over-subscribed, like the block
+// steps' larger chunks), and 14-20% on 32x32's first pass.
+constexpr int kSlotBatchSmall = 2;
+constexpr int64_t kSmallSlotPassBytes = (int64_t)256 << 20;
 
-template <typename T, int VEC>
+template <typename T, int VEC, int BATCH>
 __global__ __launch_bounds__(64 * kSlotWaves) void slot_step_kernel(T* __restrict__ out,
                                                                    const T* __restrict__ in,
                                                                    SlotArgs a) {
@@ -107,12 +114,12 @@ __global__ __launch_bounds__(64 * kSlotWaves) void slot_step_kernel(T* __restric
                                               (int64_t)kSlotChunks * 64 * VEC) *
                                        (int64_t)sizeof(T));
     const uint32_t off = (uint32_t)(threadIdx.x & 63) * VEC * (uint32_t)sizeof(T);
-    // outputs in batches of kSlotBatch: all loads of a batch are issued before its stores
-    for (int k0 = 0; k0 < a.nout[c]; k0 += kSlotBatch) {
-        V vo[kSlotBatch][kSlotChunks], vl[kSlotBatch][kSlotChunks], vr[kSlotBatch][kSlotChunks];
-        int so[kSlotBatch], sl[kSlotBatch], sr[kSlotBatch];
+    // outputs in batches of BATCH: all loads of a batch are issued before its stores
+    for (int k0 = 0; k0 < a.nout[c]; k0 += BATCH) {
+        V vo[BATCH][kSlotChunks], vl[BATCH][kSlotChunks], vr[BATCH][kSlotChunks];
+        int so[BATCH], sl[BATCH], sr[BATCH];
 #pragma unroll
-        for (int b = 0; b < kSlotBatch; ++b) {
+        for (int b = 0; b < BATCH; ++b) {
             const bool live = k0 + b < a.nout[c];
             so[b] = live ? a.own[c][k0 + b] : -1;
             sl[b] = live ? a.left[c][k0 + b] : -1;
@@ -127,7 +134,7 @@ __global__ __launch_bounds__(64 * kSlotWaves) void slot_step_kernel(T* __restric
             }
         }
 #pragma unroll
-        for (int b = 0; b < kSlotBatch; ++b) {
+        for (int b = 0; b < BATCH; ++b) {
             if (k0 + b >= a.nout[c]) break;
 #pragma unroll
             for (int u = 0; u < kSlotChunks; ++u) {
@@ -208,14 +215,22 @@ int run_slot_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, T* ws, 
             a.f_side[d] = make_fastdiv32((uint32_t)a.side[d]);
             a.f_stride[d] = make_fastdiv32((uint32_t)a.stride[d]);
         }
+        int most = 0;  // output partials of the pass, most over the collectives
+        for (int c = 0; c < p->D; ++c) most = std::max(most, a.nout[c]);
+        const bool small = most <= kSlotBatchSmall &&
+                           trivance_pass_bytes(p, elems, TRIVANCE_F32, pi) <= kSmallSlotPassBytes;
         const T* in = pi == 0 ? buf : ws + ((pi - 1) % 2) * half;
         T* out = (pi == S - 1 && S > 1) ? buf : ws + (pi % 2) * half;
         hipError_t err = hipSuccess;
         const uint64_t wgs = ((uint64_t)a.units + kSlotWaves - 1) / kSlotWaves;
         for_each_dispatch(wgs, 64 * kSlotWaves, x.items, [&](uint32_t first, uint32_t count) {
             a.wg_base = first;
-            hipLaunchKernelGGL((slot_step_kernel<T, VEC>), dim3(count), dim3(64 * kSlotWaves), 0,
-                               x.stream, out, in, a);
+            if (small)
+                hipLaunchKernelGGL((slot_step_kernel<T, VEC, kSlotBatchSmall>), dim3(count),
+                                   dim3(64 * kSlotWaves), 0, x.stream, out, in, a);
+            else
+                hipLaunchKernelGGL((slot_step_kernel<T, VEC, kSlotBatch>), dim3(count),
+                                   dim3(64 * kSlotWaves), 0, x.stream, out, in, a);
             err = hipGetLastError();
             return err == hipSuccess;
         });
