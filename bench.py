@@ -51,9 +51,9 @@ MEASURED_TRAFFIC = {
     ("torus9x9x9_B_128MiB", "block_step_kernel<copy>"): {
         "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 24427297009},
     ("ring64_L_8MiB", "slot_step_kernel"): {
-        "src": "slot.hip", "src_sha": "3d77914cd8c3b7e8", "bytes_per_launch": 3233236820},
+        "src": "slot.hip", "src_sha": "2693a8a624b314e0", "bytes_per_launch": 3233243988},
     ("torus32x32_L_8MiB", "slot_step_kernel"): {
-        "src": "slot.hip", "src_sha": "3d77914cd8c3b7e8", "bytes_per_launch": 94305433906},
+        "src": "slot.hip", "src_sha": "2693a8a624b314e0", "bytes_per_launch": 94333359694},
 }
 
 

@@ -55,11 +55,13 @@ constexpr int kSlotWaves = 4;   // waves per workgroup
 constexpr int kSlotChunks = 1;  // 64-vector chunks of one partial per wave
 constexpr int kSlotGroup = 64;  // consecutive column blocks of one rank in consecutive units
 constexpr int kSlotBatch = 4;   // output partials whose loads are issued together
-// Passes whose bytes fit in the 256 MB last-level cache (MALL) and that write at most two partials
-// per collective take batches of two: 40 instead of 63 VGPRs, so 12 waves per SIMD instead of 8.
-// On the rings of 2, 4 and 8 at 96-288 MiB per pass that measured 4-11% faster per pass, but
-// larger passes with two outputs measured 4-16% slower with it (over-subscribed, like the block
-// steps' larger chunks), and 14-20% on 32x32's first pass.
+// A pass after the first whose bytes fit in the 256 MB last-level cache (MALL) and that writes at
+// most two partials per collective takes batches of two: 40 instead of 63 VGPRs, so 12 waves per
+// SIMD instead of 8. It reads the partials the previous pass has just written (kept in the cache
+// by the SC1 store policy), and on the rings of 4 and 8 at 96-288 MiB per pass it measured 8-15%
+// faster. A first pass reads the caller's rows from HBM: there, and on passes with two outputs
+// above 256 MiB, batches of two measured 4-16% slower (over-subscribed, like the block steps'
+// larger chunks), and 14-20% on 32x32's first pass.
 constexpr int kSlotBatchSmall = 2;
 constexpr int64_t kSmallSlotPassBytes = (int64_t)256 << 20;
 
@@ -217,7 +219,7 @@ int run_slot_passes_vec(T* buf, int64_t elems, const trivance_plan_t* p, T* ws, 
         }
         int most = 0;  // output partials of the pass, most over the collectives
         for (int c = 0; c < p->D; ++c) most = std::max(most, a.nout[c]);
-        const bool small = most <= kSlotBatchSmall &&
+        const bool small = pi > 0 && most <= kSlotBatchSmall &&
                            trivance_pass_bytes(p, elems, TRIVANCE_F32, pi) <= kSmallSlotPassBytes;
         const T* in = pi == 0 ? buf : ws + ((pi - 1) % 2) * half;
         T* out = (pi == S - 1 && S > 1) ? buf : ws + (pi % 2) * half;
