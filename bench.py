@@ -46,14 +46,58 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 # the kernel source it was measured on (sha256 of that source file, first 16 hex digits); the
 # summaries are profiles/<kernel>_<workload>.md.
 MEASURED_TRAFFIC = {
+    ("ring243_B_32MiB", "block_step_kernel<reduce>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 3248038769},
+    ("ring243_B_32MiB", "block_step_kernel<copy>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 2436096862},
+    ("ring243_Bp_32MiB", "block_step_kernel<reduce>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 3248046986},
+    ("ring243_Bp_32MiB", "block_step_kernel<copy>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 2436110148},
+    ("torus27x27_B_4MiB", "block_step_kernel<reduce>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 1017880301},
+    ("torus27x27_B_4MiB", "block_step_kernel<copy>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 763434309},
+    ("torus27x27_Bp_4MiB", "block_step_kernel<reduce>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 1017886445},
+    ("torus27x27_Bp_4MiB", "block_step_kernel<copy>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 763454489},
     ("torus9x9x9_B_128MiB", "block_step_kernel<reduce>"): {
         "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 32569005959},
     ("torus9x9x9_B_128MiB", "block_step_kernel<copy>"): {
         "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 24427297009},
+    ("torus9x9x9_Bp_128MiB", "block_step_kernel<reduce>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 32568970997},
+    ("torus9x9x9_Bp_128MiB", "block_step_kernel<copy>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 24427303559},
+    ("ring81_L_8MiB", "latency_split_kernel"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 1358961457},
     ("ring64_L_8MiB", "slot_step_kernel"): {
         "src": "slot.hip", "src_sha": "2693a8a624b314e0", "bytes_per_launch": 3233243988},
+    ("ring8_L_8MiB", "slot_step_kernel"): {
+        "src": "slot.hip", "src_sha": "2693a8a624b314e0", "bytes_per_launch": 201398897},
     ("torus32x32_L_8MiB", "slot_step_kernel"): {
         "src": "slot.hip", "src_sha": "2693a8a624b314e0", "bytes_per_launch": 94333359694},
+    ("ring64_B_8MiB", "tree_step_kernel<reduce>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 283157990},
+    ("ring64_B_8MiB", "tree_step_kernel<copy>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 207665478},
+    ("ring8_B_32MiB", "tree_step_kernel<reduce>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 251701844},
+    ("ring8_B_32MiB", "tree_step_kernel<copy>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 184596997},
+    ("torus16x16x16_B_8MiB", "tree_step_kernel<reduce>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 9723961811},
+    ("torus16x16x16_B_8MiB", "tree_step_kernel<copy>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 6770476523},
+    ("torus32x32_B_8MiB", "tree_step_kernel<reduce>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 2286938665},
+    ("torus32x32_B_8MiB", "tree_step_kernel<copy>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 1679844735},
+    ("torus8x64_B_8MiB", "tree_step_kernel<reduce>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 1550511409},
+    ("torus8x64_B_8MiB", "tree_step_kernel<copy>"): {
+        "src": "executor.hip", "src_sha": "4fae51c83bf720a1", "bytes_per_launch": 1132502565},
 }
 
 

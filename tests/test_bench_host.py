@@ -69,3 +69,21 @@ def test_cpu_baseline_repeats_short_samples(name):
     assert 1 <= out["runs"] <= 3 and out["matches_gpu_on_sample"] is True
     assert out["value"] > 0 and out["cores"] == 1 and f"{out['runs']} run(s)" in out["sample"]
     assert out["gpu_fp64_bound_ratio_on_sample"] <= 1.0
+
+
+@pytest.mark.parametrize("key", sorted(bench.MEASURED_TRAFFIC), ids=lambda k: f"{k[0]}-{k[1]}")
+def test_measured_traffic_matches_the_workload(key):
+    """Each stored counter figure belongs to its workload and kernel family: within 5% of that
+    family's algorithmic bytes per launch computed from the plan (the profiles show 0.9999 to
+    1.022), so an entry keyed to the wrong workload or family fails."""
+    name, kernel = key
+    w = inputs.WORKLOADS[name]
+    plan = T.trivance_plan(w.dims, w.variant, w.placement)
+    phases = [T.trivance_plan_step(plan, p)[0] for p in range(plan.num_passes)]
+    want = 0 if kernel in ("latency_split_kernel", "slot_step_kernel") else (
+        1 if kernel.endswith("<reduce>") else 2)
+    passes = [p for p in range(plan.num_passes) if phases[p] == want]
+    assert passes, f"{name} has no pass of the {kernel} family"
+    alg = sum(T.trivance_pass_bytes(plan, w.elems, p) for p in passes) / len(passes)
+    ratio = bench.MEASURED_TRAFFIC[key]["bytes_per_launch"] / alg
+    assert 0.99 <= ratio <= 1.05, f"{name} {kernel}: traffic / algorithmic = {ratio:.4f}"
