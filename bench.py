@@ -522,7 +522,7 @@ def summary_line(w, dtype, steps=10, warmup=2, with_cpu=True):
 
 def copy_ceiling(nbytes: int = 1 << 30, reps: int = 10) -> dict:
     """The practical HBM ceiling in the same run: the library's plain streaming copy
-    (trivance_copy_device, one 16-byte non-temporal load and store per lane) of `nbytes`, timed
+    (trivance_copy_device, one 16-byte streaming load and store per lane) of `nbytes`, timed
     with HIP events on the stream it runs on. Bytes counted: read + written."""
     import torch
 

@@ -347,9 +347,10 @@ int trivance_fill_hash_uniform(void* buffers, int n, int64_t elems, uint64_t see
 
 /*
  * trivance_copy_device -- benchmark helper (not part of the AllReduce): copies `bytes` bytes from
- * device memory `src` to device memory `dst` with a plain streaming kernel (one 16-byte
- * non-temporal load and store per lane, one-wave workgroups), the simplest kernel with the step
- * kernels' access granularity. Its rate is the practical HBM ceiling reported beside them.
+ * device memory `src` to device memory `dst` with a plain streaming kernel (per lane one 16-byte
+ * non-temporal load and one streaming store with the cache policy of the step kernels' large
+ * passes, one-wave workgroups), the simplest kernel with the step kernels' access granularity.
+ * Its rate is the practical HBM ceiling reported beside them.
  * Asynchronous on stream. EINVAL unless bytes >= 0, bytes % 16 == 0, both pointers are 16-byte
  * aligned and the two ranges do not overlap; bytes == 0 does nothing.
  */
